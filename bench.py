@@ -1,0 +1,189 @@
+"""Benchmark of the sharded expert-FFN MoE layer on one MI355X.
+
+One step = one full layer forward (route -> dispatch -> expert FFN shard -> combine) over
+one batch of synthetic tokens already resident in HBM.  Prints one JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--config c2] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_F32_TFLOPS = 157.3
+FFN_SOURCES = ["paper_2503_08467_amd/csrc/ffn.hip", "paper_2503_08467_amd/csrc/common.h"]
+
+
+def ffn_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in FFN_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(config: str):
+    """HBM bytes per FFN call from the committed rocprofv3 counter summary, if it was taken
+    on the current FFN source; else None."""
+    path = os.path.join(ROOT, "profiles", f"ffn_traffic_{config}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    if rec.get("ffn_source_hash") != ffn_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_call")
+
+
+def cpu_baseline(cfg_name: str, seed: int, budget_s: float = 12.0):
+    """The fp64 oracle on a bounded sample of the same workload (its first tokens)."""
+    import oracle
+    cfg = synth.CONFIGS[cfg_name]
+    L = synth.make(cfg_name, seed=seed)
+
+    def run(n):
+        x = L.x[:n]
+        bias = None if L.sel_bias is None else L.sel_bias[:n]
+        t0 = time.perf_counter()
+        idx, w, _ = oracle.route(x, L.wg, cfg.k, bias, cfg.renorm)
+        _, offsets, row_src, pos_of = oracle.dispatch(idx, cfg.E)
+        y_perm = oracle.expert_ffn(x[row_src], offsets, L.w1, L.w3, L.w2, cfg.act)
+        oracle.combine(y_perm, pos_of, w)
+        return time.perf_counter() - t0
+
+    n = min(cfg.T, 64)
+    dt = run(n)
+    while dt < budget_s / 4 and n < cfg.T:
+        n = min(cfg.T, max(2 * n, int(n * (budget_s / 2) / max(dt, 1e-3))))
+        dt = run(n)
+    return {"value": n / dt, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"first {n} of {cfg.T} tokens of workload {cfg_name}, full layer "
+                      f"(route, dispatch, expert FFN, combine) in fp64, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="c2")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this layer's multi-GPU exchange is not built, so only "
+              "--gpus 1 is supported", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2503_08467_amd as moe
+
+    cfg = synth.CONFIGS[args.config]
+    L = synth.make(cfg, seed=args.seed)
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    to = lambda a, d=dt: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(d)
+    x, wg = to(L.x), to(L.wg)
+    bias = to(L.sel_bias, torch.float32)
+    packed = moe.pack_weights(to(L.w1), to(L.w2), to(L.w3), act=cfg.act)
+    layer = moe.MoEShardLayer(wg, packed, cfg.k, bool(cfg.renorm), max_tokens=cfg.T)
+    del L.w1, L.w2, L.w3
+
+    stream = torch.cuda.current_stream(dev)
+    nev = 5
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
+
+    def step(ev=None):
+        T, k = cfg.T, cfg.k
+        if ev: ev[0].record(stream)
+        moe.route(x, wg, k, bias, bool(cfg.renorm), out=(layer.idx, layer.w))
+        if ev: ev[1].record(stream)
+        moe.dispatch(layer.idx, x, cfg.E, out=layer.disp, ws=layer.dws)
+        if ev: ev[2].record(stream)
+        moe.expert_ffn_shard(layer.disp.x_perm, layer.disp.offsets, packed, A_max=T * k, out=layer.y_perm,
+                             ws=layer.fws)
+        if ev: ev[3].record(stream)
+        moe.combine(layer.y_perm, layer.disp.pos_of, layer.w, out=layer.y)
+        if ev: ev[4].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    stage = np.zeros(4)
+    for ev in events:
+        for s in range(4):
+            stage[s] += ev[s].elapsed_time(ev[s + 1])
+    stage_us = stage / args.steps * 1e3
+    ms_per_step = wall / args.steps * 1e3
+    tokens_per_s = cfg.T * args.steps / wall
+
+    counts = layer.disp.counts.cpu().numpy()
+    A, h, f = cfg.A, cfg.h, cfg.f
+    n_m = 3 if cfg.act == "swiglu" else 2
+    es = 2 if cfg.dtype == "bf16" else 4
+    touched = int((counts > 0).sum())
+    ffn_flops = 2.0 * n_m * A * h * f
+    ffn_bytes = n_m * h * f * es * touched + 2 * A * h * es
+    ffn_s = stage_us[2] * 1e-6
+    achieved_gbs = ffn_bytes / ffn_s / 1e9
+    achieved_tflops = ffn_flops / ffn_s / 1e12
+    peak_tf = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
+    hbm_bound = ffn_bytes / (PEAK_HBM_GBS * 1e9) > ffn_flops / (peak_tf * 1e12)
+    roof = ({"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+             "frac": round(achieved_gbs / PEAK_HBM_GBS, 4)} if hbm_bound else
+            {"bound": "mfma", "achieved": round(achieved_tflops, 1), "peak": peak_tf, "unit": "TFLOP/s",
+             "frac": round(achieved_tflops / peak_tf, 4)})
+    roof["traffic"] = measured_traffic(args.config)
+    roof["kernel"] = "moe_expert_ffn_shard (grouped GEMM1+act and GEMM2, one launch each)"
+    roof["algorithmic"] = {"bytes": ffn_bytes, "flops": ffn_flops, "touched_experts": touched,
+                           "mfma_util": round(achieved_tflops / peak_tf, 4),
+                           "hbm_frac": round(achieved_gbs / PEAK_HBM_GBS, 4)}
+
+    out = {
+        "metric": "MoE-layer tokens/sec on 1 MI355X; expert-GEMM MFMA util vs peak",
+        "value": round(tokens_per_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: T={cfg.T} h={cfg.h} E={cfg.E} top-{cfg.k} inner {cfg.f} of {cfg.F} "
+                               f"({cfg.act}), routing {cfg.routing[0]}",
+                   "tokens": cfg.T, "hidden": h, "experts": cfg.E, "top_k": cfg.k, "shard_inner_width": f,
+                   "parallelism": "single device"},
+        "stages_us": {"route": round(stage_us[0], 2), "dispatch": round(stage_us[1], 2),
+                      "expert_ffn": round(stage_us[2], 2), "combine": round(stage_us[3], 2)},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.config, args.seed)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,161 @@
+/*
+ * moeshard.h -- C ABI of the sharded expert-FFN MoE layer for AMD Instinct MI355X (gfx950).
+ *
+ * The layer is the one the MoEShard paper ("Accelerating MoE Model Inference with Expert
+ * Sharding", EuroMLSys '25) speeds up: every device holds a contiguous slice of the FFN
+ * inner width of *every* expert -- columns of W_i and the matching rows of W_o (Section
+ * 3.2) -- so it runs every expert on every token routed to it, and the devices' partial
+ * outputs sum to the unsharded result.  On one device the forward pass of Algorithm 1
+ * reduces to four calls made in order on one stream:
+ *
+ *   moe_route            Step 1, token routing (Section 3.1)
+ *   moe_dispatch         Step 2, group tokens per expert and count them (Section 3.1)
+ *   moe_expert_ffn_shard Step 4, this device's shard of every expert on its tokens, as
+ *                        one grouped computation over all experts (Sections 3.2 and 3.3)
+ *   moe_combine          Step 5, point-wise gate-weighted sum of each token's results
+ *
+ * plus moe_pack_weights, the one-time loadShard of Step 4.
+ *
+ * Conventions shared by every call
+ *  - Every data pointer is caller-owned DEVICE memory (e.g. allocated by torch); the
+ *    library never allocates, frees or keeps per-call state.  Scratch memory comes from
+ *    the caller, sized by the *_workspace_size queries.
+ *  - Every call is asynchronous on `stream` (0 = the null stream) and never synchronises
+ *    the host.  Per-expert counts stay on the device.
+ *  - Arguments are validated before anything is launched.  On an error nothing is
+ *    launched and no output is written.  Status codes: see moe_status.
+ *  - Matrices are row-major.  bf16 tensors hold raw bfloat16 bit patterns (uint16).
+ *  - Alignment: every tensor pointer must be 16-byte aligned.
+ *  - Limits: 1 <= k <= E <= MOE_MAX_EXPERTS; h >= 8 and h % 8 == 0; T * k < 2^31.
+ *  - Outputs are bitwise deterministic: no floating-point atomics, fixed reduction order.
+ *  - Calls on different streams that share no output buffers may run concurrently.
+ */
+#ifndef MOESHARD_H
+#define MOESHARD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOE_MAX_EXPERTS 256
+
+typedef enum {
+    MOE_OK = 0,
+    MOE_ERR_INVALID_ARG = 1, /* a size, pointer, alignment or enum value is invalid */
+    MOE_ERR_UNSUPPORTED = 2, /* valid request this build does not implement */
+    MOE_ERR_WORKSPACE = 3,   /* the workspace or packed buffer is too small */
+    MOE_ERR_HIP = 4          /* the HIP runtime reported a launch error */
+} moe_status;
+
+typedef enum { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype;
+
+/* Activation between the two expert matrices.  The paper writes the expert as two
+ * matmuls (Section 3.2) and never names the activation; any element-wise activation
+ * keeps the shard-sum property, because it acts on each inner column independently.
+ *   MOE_ACT_GELU       u * Phi(u)                          (erf form)
+ *   MOE_ACT_GELU_TANH  0.5 u (1 + tanh(sqrt(2/pi) (u + 0.044715 u^3)))
+ *   MOE_ACT_SWIGLU     silu(x W1) * (x W3), W1 and W3 sliced on the same inner columns */
+typedef enum { MOE_ACT_GELU = 0, MOE_ACT_GELU_TANH = 1, MOE_ACT_SWIGLU = 2 } moe_act;
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char *moe_status_string(moe_status status);
+
+/* Step 1 (Algorithm 1, token routing; Section 3.1: the router maps each token to its
+ * expert(s)).
+ *   x         [T, h]  activations, dtype xdt (MOE_BF16 or MOE_F32)
+ *   w_gate    [E, h]  gate projection, dtype xdt; row e is expert e's gate vector
+ *   sel_bias  nullable fp32 selection bias: bias_row_stride == 0 -> [E] shared by all
+ *             tokens, bias_row_stride == E -> [T, E] per token
+ *   renorm    0: weights are the softmax probabilities; 1: divided by their sum over k
+ *   topk_idx  [T, k] int32 out: expert ids in decreasing order of logit + bias; equal
+ *             scores go to the lower expert id
+ *   topk_w    [T, k] fp32 out: softmax of the UNBIASED logits (fp32 accumulation) at the
+ *             picked experts; the bias only changes which experts are picked
+ * T == 0 is a valid no-op. */
+moe_status moe_route(const void *x, moe_dtype xdt, int64_t T, int64_t h, const void *w_gate,
+                     int32_t E, int32_t k, const float *sel_bias, int64_t bias_row_stride,
+                     int32_t renorm, int32_t *topk_idx, float *topk_w, hipStream_t stream);
+
+/* Bytes of workspace moe_dispatch needs for T tokens, k picks and E experts. */
+size_t moe_dispatch_workspace_size(int64_t T, int32_t k, int32_t E);
+
+/* Step 2 (Algorithm 1, groupPerExpert and countPerExpert; Section 3.1).  The A = T*k
+ * assignments (t, j) are grouped by expert; inside a group they keep (t, j) order.
+ *   topk_idx  [T, k] int32 expert ids; an id outside [0, E) is dropped: it is not
+ *             counted, gets pos_of = -1 and contributes nothing in moe_combine
+ *   x         [T, h] rows to permute, dtype xdt
+ *   counts    [E]   out: assignments per expert (m_sizes of the paper)
+ *   offsets   [E+1] out: exclusive prefix sum of counts; offsets[E] = A when every id
+ *             is valid
+ *   row_src   [A]   out: token of the assignment at grouped position p
+ *   pos_of    [T,k] out: grouped position of assignment (t, j)
+ *   x_perm    [A, h] out: x_perm[p] = x[row_src[p]], bit copies
+ *   ws        moe_dispatch_workspace_size(T, k, E) bytes, 16-byte aligned
+ * T == 0 writes zero counts and offsets. */
+moe_status moe_dispatch(const int32_t *topk_idx, int64_t T, int32_t k, int32_t E,
+                        const void *x, moe_dtype xdt, int64_t h, int32_t *counts,
+                        int32_t *offsets, int32_t *row_src, int32_t *pos_of, void *x_perm,
+                        void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Inner width after padding to the grouped GEMM's tile multiple (the packed layout). */
+int64_t moe_padded_inner_width(int64_t f);
+
+/* Bytes of the packed shard for E experts, hidden h, shard inner width f. */
+size_t moe_packed_weights_size(int32_t E, int64_t h, int64_t f, moe_act act, moe_dtype wdt);
+
+/* loadShard of Step 4: cut this device's shard out of full expert weights and lay it out
+ * for the grouped GEMM (Section 3.2: W_i split by columns, W_o by the matching rows; the
+ * shard is the contiguous inner slice [col0, col0 + f)).
+ *   w1  [E, h, F]  W_i of every expert, dtype wdt (SwiGLU: the gate projection)
+ *   w3  [E, h, F]  SwiGLU up projection (same columns), NULL otherwise
+ *   w2  [E, F, h]  W_o of every expert
+ *   0 <= col0, f >= 1, col0 + f <= F
+ *   packed  moe_packed_weights_size(...) bytes.  Layout (internal, may change):
+ *           W1^T [E][fp][h], (W3^T [E][fp][h]), W2^T [E][h][fp], fp = padded f;
+ *           padded inner columns are zero, which is exact: every activation maps 0 to 0.
+ * Run once per shard; the result is read-only for moe_expert_ffn_shard. */
+moe_status moe_pack_weights(const void *w1, const void *w3, const void *w2, int32_t E,
+                            int64_t h, int64_t F, int64_t col0, int64_t f, moe_act act,
+                            moe_dtype wdt, void *packed, size_t packed_bytes,
+                            hipStream_t stream);
+
+/* Bytes of workspace moe_expert_ffn_shard needs (the activated inner rows). */
+size_t moe_ffn_workspace_size(int64_t A_max, int32_t E, int64_t h, int64_t f, moe_act act,
+                              moe_dtype dt);
+
+/* Step 4 (Algorithm 1, expert computation; Section 3.3's single grouped operation over
+ * all experts): for every expert e and every grouped row p in [offsets[e], offsets[e+1]):
+ *     y_perm[p] = act(x_perm[p] . W1_e^g) . W2_e^g        (shard g = the packed slice)
+ * computed with bf16 MFMA and fp32 accumulation (dt = MOE_BF16) or fp32 arithmetic
+ * (dt = MOE_F32).  The activated row is rounded to dt before the second product.  One
+ * launch per matmul regardless of E; the per-expert counts are read on the device.
+ *   x_perm  [A, h] dtype dt, grouped rows from moe_dispatch
+ *   offsets [E+1] int32, device; offsets[E] must not exceed A_max
+ *   A_max   host-known upper bound of offsets[E] (normally T*k); sizes the launch
+ *   packed  from moe_pack_weights with the same E, h, f, act and dt
+ *   y_perm  [A, h] out, dtype ydt (MOE_F32 keeps an unrounded shard partial)
+ *   ws      moe_ffn_workspace_size(A_max, E, h, f, act, dt) bytes */
+moe_status moe_expert_ffn_shard(const void *x_perm, const int32_t *offsets, int64_t A_max,
+                                int32_t E, int64_t h, int64_t f, moe_act act, moe_dtype dt,
+                                const void *packed, void *y_perm, moe_dtype ydt, void *ws,
+                                size_t ws_bytes, hipStream_t stream);
+
+/* Step 5 (Algorithm 1, aggregateTokens): point-wise weighted sum of each token's expert
+ * results, accumulated in fp32 in pick order j = 0..k-1 and rounded once:
+ *     y[t] = sum_j topk_w[t, j] * y_perm[pos_of[t, j]]
+ *   y_perm [A, h] dtype ydt; pos_of [T, k] (negative entries are skipped); topk_w [T, k]
+ *   fp32; y [T, h] out, dtype out_dt */
+moe_status moe_combine(const void *y_perm, moe_dtype ydt, const int32_t *pos_of,
+                       const float *topk_w, int64_t T, int32_t k, int64_t h, void *y,
+                       moe_dtype out_dt, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOESHARD_H */

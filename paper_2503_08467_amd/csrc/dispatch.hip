@@ -1,0 +1,195 @@
+// Step 2 of the layer: count the assignments per expert, scan, and group them stably.
+//
+//   count   one workgroup per chunk of kDispatchChunk assignments builds an LDS histogram
+//           and writes it expert-major: cc[e * nchunks + c]
+//   scan    one workgroup scans cc in that order; the exclusive prefix at (e, c) is the
+//           first grouped position of chunk c's expert-e assignments, and at (e, 0) it is
+//           offsets[e]
+//   rank    per chunk, each wave walks its 256 assignments in 4 rounds of 64; lanes with
+//           the same expert find each other with ballots over the id bits, so an
+//           assignment's position is   chunk base + earlier waves' count + running count
+//           + number of lower lanes with the same expert   -- stable in (t, j) order
+//   gather  x_perm[p] = x[row_src[p]] with 16-byte vector copies
+// Integer atomics are used only for the LDS histogram, whose result does not depend on
+// their order.
+#include "common.h"
+#include "kernels.h"
+
+#include "../../include/moeshard.h"
+
+namespace moe {
+namespace {
+
+constexpr int kDispThreads = 256;
+constexpr int kDispWaves = kDispThreads / kWave;
+constexpr int kPerWave = kDispatchChunk / kDispWaves;  // 256
+constexpr int kRounds = kPerWave / kWave;              // 4
+
+__global__ __launch_bounds__(kDispThreads) void dispatch_count(const int32_t* __restrict__ idx, int64_t A,
+                                                               int E, int nchunks, int32_t* __restrict__ cc) {
+    __shared__ int hist[MOE_MAX_EXPERTS];
+    for (int e = threadIdx.x; e < E; e += kDispThreads) hist[e] = 0;
+    __syncthreads();
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kDispatchChunk;
+    for (int i = threadIdx.x; i < kDispatchChunk; i += kDispThreads) {
+        const int64_t a = base + i;
+        if (a < A) {
+            const int e = idx[a];
+            if (static_cast<unsigned>(e) < static_cast<unsigned>(E)) atomicAdd(&hist[e], 1);
+        }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < E; e += kDispThreads)
+        cc[static_cast<int64_t>(e) * nchunks + blockIdx.x] = hist[e];
+}
+
+constexpr int kScanThreads = 1024;
+
+__global__ __launch_bounds__(kScanThreads) void dispatch_scan(const int32_t* __restrict__ cc, int E,
+                                                              int nchunks, int32_t* __restrict__ base,
+                                                              int32_t* __restrict__ counts,
+                                                              int32_t* __restrict__ offsets) {
+    __shared__ int part[kScanThreads];
+    __shared__ int off[MOE_MAX_EXPERTS + 1];
+    const int tid = threadIdx.x;
+    const int64_t L = static_cast<int64_t>(E) * nchunks;
+    for (int e = tid; e <= E; e += kScanThreads) off[e] = 0;
+    const int64_t per = ceil_div(L, kScanThreads);
+    const int64_t lo = tid * per;
+    const int64_t hi = (lo + per < L) ? lo + per : L;
+    int sum = 0;
+    for (int64_t i = lo; i < hi; ++i) sum += cc[i];
+    part[tid] = sum;
+    __syncthreads();
+    for (int o = 1; o < kScanThreads; o <<= 1) {
+        const int v = (tid >= o) ? part[tid - o] : 0;
+        __syncthreads();
+        part[tid] += v;
+        __syncthreads();
+    }
+    int run = part[tid] - sum;
+    for (int64_t i = lo; i < hi; ++i) {
+        if (i % nchunks == 0) off[i / nchunks] = run;
+        base[i] = run;
+        run += cc[i];
+    }
+    if (tid == 0) off[E] = part[kScanThreads - 1];
+    __syncthreads();
+    for (int e = tid; e <= E; e += kScanThreads) {
+        offsets[e] = off[e];
+        if (e < E) counts[e] = off[e + 1] - off[e];
+    }
+}
+
+__global__ __launch_bounds__(kDispThreads) void dispatch_rank(const int32_t* __restrict__ idx, int64_t A,
+                                                              int k, int E, int nbits, int nchunks,
+                                                              const int32_t* __restrict__ base,
+                                                              int32_t* __restrict__ row_src,
+                                                              int32_t* __restrict__ pos_of) {
+    __shared__ int wcnt[kDispWaves][MOE_MAX_EXPERTS];
+    __shared__ int run[kDispWaves][MOE_MAX_EXPERTS];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int c = blockIdx.x;
+    for (int e = lane; e < E; e += kWave) wcnt[wave][e] = 0;
+    __syncthreads();
+    const int64_t a0 = static_cast<int64_t>(c) * kDispatchChunk + wave * kPerWave;
+    int ev[kRounds];
+#pragma unroll
+    for (int s = 0; s < kRounds; ++s) {
+        const int64_t a = a0 + s * kWave + lane;
+        ev[s] = (a < A) ? idx[a] : -1;
+        if (static_cast<unsigned>(ev[s]) < static_cast<unsigned>(E)) atomicAdd(&wcnt[wave][ev[s]], 1);
+    }
+    __syncthreads();
+    for (int e = lane; e < E; e += kWave) {
+        int b = base[static_cast<int64_t>(e) * nchunks + c];
+        for (int w = 0; w < wave; ++w) b += wcnt[w][e];
+        run[wave][e] = b;
+    }
+    __syncthreads();
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
+    for (int s = 0; s < kRounds; ++s) {
+        const int64_t a = a0 + s * kWave + lane;
+        const int e = ev[s];
+        const bool valid = static_cast<unsigned>(e) < static_cast<unsigned>(E);
+        uint64_t peers = __ballot(valid);
+        for (int b = 0; b < nbits; ++b) {
+            const bool bit = valid && ((e >> b) & 1);
+            const uint64_t m = __ballot(bit);
+            peers &= bit ? m : ~m;
+        }
+        const int rank = __popcll(peers & lt);
+        if (valid) {
+            const int pos = run[wave][e] + rank;
+            pos_of[a] = pos;
+            if (pos >= 0 && pos < A) row_src[pos] = static_cast<int32_t>(a / k);
+        } else if (a < A) {
+            pos_of[a] = -1;
+        }
+        __syncthreads();  // every lane has read run[] before the group leaders advance it
+        if (valid && rank == 0) run[wave][e] += __popcll(peers);
+        __syncthreads();
+    }
+}
+
+// x_perm[p] = x[row_src[p]] for p < offsets[E]; each thread moves kGatherUnroll 16-byte vectors.
+constexpr int kGatherUnroll = 4;
+
+__global__ __launch_bounds__(256) void dispatch_gather(const uint4* __restrict__ x,
+                                                       const int32_t* __restrict__ row_src,
+                                                       const int32_t* __restrict__ offsets, int E,
+                                                       uint32_t A_cap, uint32_t T, uint32_t nvec,
+                                                       uint4* __restrict__ x_perm) {
+    const uint32_t A = min(static_cast<uint32_t>(offsets[E]), A_cap);
+    const uint64_t total = static_cast<uint64_t>(A) * nvec;
+    const uint64_t i0 = (static_cast<uint64_t>(blockIdx.x) * 256 * kGatherUnroll) + threadIdx.x;
+    uint4 v[kGatherUnroll];
+    uint64_t dst[kGatherUnroll];
+#pragma unroll
+    for (int u = 0; u < kGatherUnroll; ++u) {
+        const uint64_t i = i0 + u * 256;
+        dst[u] = i;
+        if (i < total) {
+            const uint32_t p = static_cast<uint32_t>(i / nvec);
+            const uint32_t col = static_cast<uint32_t>(i - static_cast<uint64_t>(p) * nvec);
+            const uint32_t src = static_cast<uint32_t>(row_src[p]);
+            v[u] = x[static_cast<uint64_t>(src < T ? src : 0) * nvec + col];
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kGatherUnroll; ++u)
+        if (dst[u] < total) x_perm[dst[u]] = v[u];
+}
+
+}  // namespace
+
+hipError_t launch_dispatch(const int32_t* idx, int64_t T, int k, int E, const void* x, int elem_bytes,
+                           int h, int32_t* counts, int32_t* offsets, int32_t* row_src,
+                           int32_t* pos_of, void* x_perm, int32_t* ws, hipStream_t s) {
+    const int64_t A = T * k;
+    const int nchunks = static_cast<int>(ceil_div(A, kDispatchChunk));
+    int32_t* cc = ws;
+    int32_t* base = ws + static_cast<int64_t>(E) * nchunks;
+    int nbits = 0;
+    while ((1 << nbits) < E) ++nbits;
+    if (nchunks > 0) {
+        hipLaunchKernelGGL(dispatch_count, dim3(nchunks), dim3(kDispThreads), 0, s, idx, A, E, nchunks, cc);
+    }
+    hipLaunchKernelGGL(dispatch_scan, dim3(1), dim3(kScanThreads), 0, s, cc, E, nchunks, base, counts,
+                       offsets);
+    if (nchunks > 0) {
+        hipLaunchKernelGGL(dispatch_rank, dim3(nchunks), dim3(kDispThreads), 0, s, idx, A, k, E, nbits,
+                           nchunks, base, row_src, pos_of);
+        const uint32_t nvec = static_cast<uint32_t>(static_cast<int64_t>(h) * elem_bytes / 16);
+        const uint64_t total = static_cast<uint64_t>(A) * nvec;
+        const uint64_t blocks = ceil_div(static_cast<int64_t>(total), 256 * kGatherUnroll);
+        hipLaunchKernelGGL(dispatch_gather, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
+                           static_cast<const uint4*>(x), row_src, offsets, E, static_cast<uint32_t>(A),
+                           static_cast<uint32_t>(T), nvec, static_cast<uint4*>(x_perm));
+    }
+    return hipGetLastError();
+}
+
+}  // namespace moe

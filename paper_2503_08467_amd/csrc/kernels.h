@@ -1,0 +1,33 @@
+// Internal launchers of the MoE layer kernels (called by the C ABI after validation).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace moe {
+
+// Tile constants shared by the packer and the grouped GEMM.
+constexpr int kInnerAlign = 128;  // packed inner width is a multiple of this
+constexpr int kDispatchChunk = 1024;  // assignments per dispatch workgroup
+
+hipError_t launch_route(const void* x, bool bf16, int64_t T, int h, const void* wg, int E, int k,
+                        const float* bias, int64_t bias_stride, int renorm, int32_t* idx, float* w,
+                        hipStream_t s);
+
+hipError_t launch_dispatch(const int32_t* idx, int64_t T, int k, int E, const void* x, int elem_bytes,
+                           int h, int32_t* counts, int32_t* offsets, int32_t* row_src,
+                           int32_t* pos_of, void* x_perm, int32_t* ws, hipStream_t s);
+
+hipError_t launch_pack(const void* w1, const void* w3, const void* w2, int E, int64_t h, int64_t F,
+                       int64_t col0, int64_t f, int64_t fp, int elem_bytes, void* w1t, void* w3t,
+                       void* w2t, hipStream_t s);
+
+hipError_t launch_ffn(const void* x_perm, const int32_t* offsets, int64_t A_max, int E, int h,
+                      int64_t fp, int act, bool bf16, const void* w1t, const void* w3t,
+                      const void* w2t, void* y_perm, bool y_bf16, void* hbuf, hipStream_t s);
+
+hipError_t launch_combine(const void* y_perm, bool y_bf16, const int32_t* pos_of, const float* w,
+                          int64_t T, int k, int h, void* y, bool out_bf16, hipStream_t s);
+
+}  // namespace moe

@@ -1,0 +1,128 @@
+"""The C ABI library loads, exports every declared symbol and rejects bad arguments on the
+host before launching anything (CPU only: every call below fails validation, so no HIP
+call is made)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2503_08467_amd as moe
+from paper_2503_08467_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moeshard.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2503_08467_amd import build
+        build.build()
+    return _lib.load()
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w]+\s*\*?\s*(moe_\w+)\s*\(", src, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert len(names) == 10, names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(_lib.SIGNATURES)
+
+
+def test_status_strings(lib):
+    for st in range(5):
+        assert _lib.status_string(st).startswith("MOE_")
+    assert "unknown" in _lib.status_string(99)
+
+
+A16 = 0x10000  # a 16-byte aligned non-null address; never dereferenced (validation fails first)
+
+
+def _route(lib, **kw):
+    a = dict(x=A16, xdt=_lib.MOE_BF16, T=8, h=64, wg=A16, E=8, k=2, bias=None, stride=0, renorm=0,
+             idx=A16, w=A16, s=None)
+    a.update(kw)
+    return lib.moe_route(*a.values())
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(k=9), _lib.MOE_ERR_INVALID_ARG),        # k > E
+    (dict(k=0), _lib.MOE_ERR_INVALID_ARG),
+    (dict(E=0, k=0), _lib.MOE_ERR_INVALID_ARG),
+    (dict(E=300, k=2), _lib.MOE_ERR_UNSUPPORTED),  # beyond MOE_MAX_EXPERTS
+    (dict(T=-1), _lib.MOE_ERR_INVALID_ARG),
+    (dict(h=60), _lib.MOE_ERR_INVALID_ARG),        # h % 8 != 0
+    (dict(xdt=7), _lib.MOE_ERR_INVALID_ARG),
+    (dict(x=A16 + 4), _lib.MOE_ERR_INVALID_ARG),   # misaligned
+    (dict(x=None), _lib.MOE_ERR_INVALID_ARG),      # null required pointer
+    (dict(stride=3), _lib.MOE_ERR_INVALID_ARG),    # bias stride neither 0 nor E
+    (dict(renorm=2), _lib.MOE_ERR_INVALID_ARG),
+])
+def test_route_rejects_bad_arguments(lib, kw, status):
+    assert _route(lib, **kw) == status
+
+
+def test_route_with_no_tokens_is_a_noop(lib):
+    assert _route(lib, T=0, x=None, idx=None, w=None) == _lib.MOE_OK
+
+
+def test_dispatch_rejects_small_workspace(lib):
+    need = lib.moe_dispatch_workspace_size(100, 2, 16)
+    assert need > 0
+    st = lib.moe_dispatch(A16, 100, 2, 16, A16, _lib.MOE_BF16, 64, A16, A16, A16, A16, A16, A16, need - 1, None)
+    assert st == _lib.MOE_ERR_WORKSPACE
+    st = lib.moe_dispatch(A16, 100, 3, 2, A16, _lib.MOE_BF16, 64, A16, A16, A16, A16, A16, A16, need, None)
+    assert st == _lib.MOE_ERR_INVALID_ARG  # k > E
+
+
+def test_pack_rejects_bad_slices(lib):
+    E, h, F = 4, 64, 100
+    size = lib.moe_packed_weights_size(E, h, 50, _lib.MOE_ACT_GELU, _lib.MOE_BF16)
+    args = lambda col0, f, w3=None, act=_lib.MOE_ACT_GELU, nbytes=size: (
+        A16, w3, A16, E, h, F, col0, f, act, _lib.MOE_BF16, A16, nbytes, None)
+    assert lib.moe_pack_weights(*args(60, 50)) == _lib.MOE_ERR_INVALID_ARG  # col0 + f > F
+    assert lib.moe_pack_weights(*args(-1, 50)) == _lib.MOE_ERR_INVALID_ARG
+    assert lib.moe_pack_weights(*args(0, 0)) == _lib.MOE_ERR_INVALID_ARG
+    assert lib.moe_pack_weights(*args(0, 50, nbytes=size - 1)) == _lib.MOE_ERR_WORKSPACE
+    assert lib.moe_pack_weights(*args(0, 50, act=_lib.MOE_ACT_SWIGLU)) == _lib.MOE_ERR_INVALID_ARG  # no w3
+
+
+def test_sizes_follow_the_padded_layout(lib):
+    assert lib.moe_padded_inner_width(1) == 128
+    assert lib.moe_padded_inner_width(512) == 512
+    assert lib.moe_padded_inner_width(1792) == 1792
+    assert lib.moe_padded_inner_width(37) == 128
+    # W1^T + W2^T (+ W3^T) of E x fp x h elements
+    assert lib.moe_packed_weights_size(8, 768, 3072, _lib.MOE_ACT_GELU, _lib.MOE_BF16) == 2 * 8 * 3072 * 768 * 2
+    assert lib.moe_packed_weights_size(8, 4096, 1792, _lib.MOE_ACT_SWIGLU, _lib.MOE_BF16) == 3 * 8 * 1792 * 4096 * 2
+    assert lib.moe_ffn_workspace_size(1000, 8, 768, 3072, _lib.MOE_ACT_GELU, _lib.MOE_F32) >= 1000 * 3072 * 4
+
+
+def test_ffn_and_combine_reject_bad_arguments(lib):
+    ws = lib.moe_ffn_workspace_size(64, 8, 64, 32, _lib.MOE_ACT_GELU, _lib.MOE_BF16)
+    ok_args = [A16, A16, 64, 8, 64, 32, _lib.MOE_ACT_GELU, _lib.MOE_BF16, A16, A16, _lib.MOE_BF16, A16, ws, None]
+    bad = list(ok_args); bad[11 + 1] = ws - 1
+    assert lib.moe_expert_ffn_shard(*bad) == _lib.MOE_ERR_WORKSPACE
+    bad = list(ok_args); bad[6] = 5
+    assert lib.moe_expert_ffn_shard(*bad) == _lib.MOE_ERR_INVALID_ARG
+    bad = list(ok_args); bad[3] = 257
+    assert lib.moe_expert_ffn_shard(*bad) == _lib.MOE_ERR_UNSUPPORTED
+    bad = list(ok_args); bad[8] = A16 + 8
+    assert lib.moe_expert_ffn_shard(*bad) == _lib.MOE_ERR_INVALID_ARG
+    assert lib.moe_combine(A16, _lib.MOE_BF16, A16, A16, 4, 0, 64, A16, _lib.MOE_BF16, None) == _lib.MOE_ERR_INVALID_ARG
+    assert lib.moe_combine(A16, _lib.MOE_BF16, A16, A16, 4, 1, 12, A16, _lib.MOE_BF16, None) == _lib.MOE_ERR_INVALID_ARG
+    assert lib.moe_combine(None, _lib.MOE_BF16, None, None, 0, 1, 64, None, _lib.MOE_BF16, None) == _lib.MOE_OK
+
+
+def test_python_binding_refuses_cpu_tensors():
+    import torch
+    x = torch.zeros(4, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        moe.route(x, torch.zeros(8, 64, dtype=torch.bfloat16), 1)

@@ -1,0 +1,330 @@
+"""GPU parity of every step of the layer against the fp64 oracle (needs an MI355X).
+
+Stage tests feed each kernel the oracle's inputs for that stage, so a failure points at
+one kernel; end-to-end tests run the whole layer on the five workloads.  Integers are
+compared bit-exactly; floats with the normwise error of each output row against the
+oracle: <= 2e-2 for bf16 paths, <= 1e-5 for the fp32 path.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from _util import by_expert, compare_routing, normwise, rowwise, to_dev
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+import paper_2503_08467_amd as moe  # noqa: E402
+
+TOL = {"bf16": 2e-2, "f32": 1e-5}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    moe.load()
+    yield
+    torch.cuda.synchronize()
+
+
+def tdt(cfg_dtype):
+    return torch.bfloat16 if cfg_dtype == "bf16" else torch.float32
+
+
+def np_of(t):
+    return t.detach().float().cpu().numpy() if t.dtype == torch.bfloat16 else t.detach().cpu().numpy()
+
+
+# ------------------------------------------------------------------------------- route
+
+def _check_route(x, wg, bias, k, renorm, dtype, exact_products):
+    dt = tdt(dtype)
+    idx, w = moe.route(to_dev(x, dt), to_dev(wg, dt), k, to_dev(bias, torch.float32), renorm)
+    torch.cuda.synchronize()
+    gi, gw = idx.cpu().numpy(), w.cpu().numpy()
+    oi, ow, logits = oracle.route(x, wg, k, bias, renorm)
+    same_set, order_ok = compare_routing(gi, gw, oi, ow, x, wg, bias, logits, k, exact_products)
+    return gi, int((~order_ok).sum())
+
+
+@pytest.mark.parametrize("name,T", [("c1", 512), ("c2", 8192), ("c3", 16384), ("c4", 4096), ("c5", 32768),
+                                    ("c5dec", 64)])
+def test_route_parity_on_workloads(name, T):
+    L = synth.make(name, seed=0, weights=False, T=T)
+    gi, unsure = _check_route(L.x, L.wg, L.sel_bias, L.cfg.k, L.cfg.renorm, L.cfg.dtype, L.cfg.dtype == "bf16")
+    print(f"{name}: {unsure} tokens within the fp32 rounding margin")
+    if L.targets is not None:  # the injected routing is exactly what the kernel picked
+        assert np.array_equal(np.sort(gi, axis=1), L.targets)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("T,h,E,k", [(1, 8, 1, 1), (17, 72, 3, 2), (100, 256, 16, 16), (65, 136, 17, 4),
+                                     (130, 64, 64, 2), (33, 512, 200, 8), (64, 96, 256, 3), (257, 1024, 128, 1)])
+@pytest.mark.parametrize("bias_kind", ["none", "row", "shared"])
+def test_route_shapes_and_bias(dtype, T, h, E, k, bias_kind):
+    rng = np.random.default_rng(T * 1000 + E)
+    x = rng.standard_normal((T, h)).astype(np.float32)
+    wg = (rng.standard_normal((E, h)) * 0.05).astype(np.float32)
+    if dtype == "bf16":
+        x, wg = synth.round_to_bf16(x), synth.round_to_bf16(wg)
+    bias = {"none": None, "row": rng.standard_normal((T, E)).astype(np.float32),
+            "shared": rng.standard_normal(E).astype(np.float32)}[bias_kind]
+    _check_route(x, wg, bias, k, int(k > 1), dtype, dtype == "bf16")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_route_exact_ties_go_to_lower_expert(dtype):
+    rng = np.random.default_rng(5)
+    T, h, E = 200, 64, 40
+    x = rng.integers(-4, 5, (T, h)).astype(np.float32)  # exact logits in fp32 and fp64
+    x[3] = 0
+    wg = rng.integers(-3, 4, (E, h)).astype(np.float32)
+    wg[30] = wg[7]
+    wg[39] = wg[0]
+    for k in (1, 5, E):
+        idx, _ = moe.route(to_dev(x, tdt(dtype)), to_dev(wg, tdt(dtype)), k)
+        oi, _, _ = oracle.route(x, wg, k)
+        assert np.array_equal(idx.cpu().numpy(), oi)
+        assert idx[3].tolist() == list(range(k))
+
+
+# ------------------------------------------------------------------------------- dispatch
+
+def _check_dispatch(idx, E, h=64, dtype=torch.bfloat16):
+    T, k = idx.shape
+    rng = np.random.default_rng(T + E)
+    xd = to_dev(rng.standard_normal((T, h)).astype(np.float32), dtype)
+    d = moe.dispatch(to_dev(idx, torch.int32), xd, E)
+    torch.cuda.synchronize()
+    gc, go, gr, gp = (d.counts.cpu().numpy(), d.offsets.cpu().numpy(), d.row_src.cpu().numpy(),
+                      d.pos_of.cpu().numpy())
+    flat = idx.ravel()
+    keep = (flat >= 0) & (flat < E)
+    if keep.all():
+        counts, offsets, row_src, pos_of = oracle.dispatch(idx, E)
+        assert np.array_equal(gc, counts)
+        assert np.array_equal(go, offsets)
+        assert np.array_equal(gr, row_src)
+        assert np.array_equal(gp, pos_of)
+    else:
+        # invalid ids are dropped: counts and order are those of the valid ids alone
+        order = np.argsort(np.where(keep, flat, E), kind="stable")[:keep.sum()]
+        assert np.array_equal(gc, np.bincount(flat[keep], minlength=E))
+        assert go[-1] == keep.sum()
+        assert np.array_equal(gr[:keep.sum()], order // k)
+        exp_pos = np.full(T * k, -1)
+        exp_pos[order] = np.arange(keep.sum())
+        assert np.array_equal(gp.ravel(), exp_pos)
+    A = int(keep.sum())
+    src = torch.from_numpy(gr[:A].astype(np.int64)).to(xd.device)
+    assert torch.equal(d.x_perm[:A], xd[src])
+
+
+@pytest.mark.parametrize("T,k,E", [(0, 1, 8), (1, 1, 1), (5, 2, 5), (1000, 1, 64), (1023, 2, 7), (1024, 2, 256),
+                                   (3000, 3, 100), (16384, 1, 128), (32768, 2, 64), (4096, 8, 256)])
+def test_dispatch_bit_exact(T, k, E):
+    rng = np.random.default_rng(T + 7 * E)
+    p = rng.dirichlet(np.full(E, 0.3))  # skewed popularity, many empty experts
+    idx = np.stack([rng.choice(E, size=k, replace=False, p=p) for _ in range(T)]).astype(np.int32) \
+        if T else np.zeros((0, k), np.int32)
+    _check_dispatch(idx, E)
+
+
+def test_dispatch_golden_example():
+    import json, os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "dispatch_worked_example.json")))
+    d = moe.dispatch(to_dev(np.array(g["idx"], np.int32), torch.int32),
+                     torch.zeros((g["T"], 16), dtype=torch.bfloat16, device="cuda"), g["E"])
+    assert d.counts.tolist() == g["counts"] and d.offsets.tolist() == g["offsets"]
+    assert d.row_src.tolist() == g["row_src"] and d.pos_of.tolist() == g["pos_of"]
+
+
+def test_dispatch_drops_invalid_ids():
+    rng = np.random.default_rng(1)
+    idx = rng.integers(0, 9, (700, 2)).astype(np.int32)
+    idx[::7, 0] = -1
+    idx[::11, 1] = 9 + 3
+    _check_dispatch(idx, 9, h=32, dtype=torch.float32)
+
+
+# ------------------------------------------------------------------------------- expert FFN
+
+def _ffn_case(rng, counts, h, f, act, dtype, F=None, col0=0):
+    E = len(counts)
+    F = F or f
+    A = int(sum(counts))
+    std = 0.05
+    x = rng.standard_normal((A, h)).astype(np.float32)
+    w1 = (rng.standard_normal((E, h, F)) * std).astype(np.float32)
+    w3 = (rng.standard_normal((E, h, F)) * std).astype(np.float32) if act == "swiglu" else None
+    w2 = (rng.standard_normal((E, F, h)) * std).astype(np.float32)
+    if dtype == "bf16":
+        x, w1, w2 = synth.round_to_bf16(x), synth.round_to_bf16(w1), synth.round_to_bf16(w2)
+        w3 = None if w3 is None else synth.round_to_bf16(w3)
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    return x, w1, w3, w2, offsets
+
+
+def _run_ffn(x, w1, w3, w2, offsets, act, dtype, out_dtype=None, col0=0, f=None):
+    dt = tdt(dtype)
+    packed = moe.pack_weights(to_dev(w1, dt), to_dev(w2, dt), to_dev(w3, dt), col0=col0, f=f, act=act)
+    y = moe.expert_ffn_shard(to_dev(x, dt), to_dev(offsets, torch.int32), packed, out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    return np_of(y)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("act", ["gelu", "gelu_tanh", "swiglu"])
+@pytest.mark.parametrize("counts,h,f", [
+    ([300, 0, 5, 129, 128, 1], 256, 200),     # ragged rows and a ragged inner width
+    ([1], 64, 37),
+    ([0, 0, 77], 72, 128),                     # h not a multiple of the 64-wide K step
+    ([513, 40, 0, 255], 768, 512),
+])
+def test_ffn_parity(dtype, act, counts, h, f):
+    rng = np.random.default_rng(sum(counts) + h + f)
+    x, w1, w3, w2, offsets = _ffn_case(rng, counts, h, f, act, dtype)
+    got = _run_ffn(x, w1, w3, w2, offsets, act, dtype)
+    ref = oracle.expert_ffn(x, offsets, w1, w3, w2, act)
+    assert rowwise(got, ref) <= TOL[dtype], (rowwise(got, ref), normwise(got, ref))
+
+
+@pytest.mark.parametrize("g", [0, 1, 2, 3])
+def test_ffn_shard_slice_of_full_weights(g):
+    """moe_pack_weights cuts shard g (inner columns [g*f, (g+1)*f)) out of the full weights;
+    the shard partials, summed over g in fp32 on the host, give the unsharded output."""
+    rng = np.random.default_rng(42)
+    F, f = 4 * 96, 96
+    x, w1, w3, w2, offsets = _ffn_case(rng, [70, 3, 0, 190], 128, F, "gelu", "bf16")
+    got = _run_ffn(x, w1, w3, w2, offsets, "gelu", "bf16", out_dtype=torch.float32, col0=g * f, f=f)
+    ref = oracle.expert_ffn(x, offsets, w1, w3, w2, "gelu", col0=g * f, f=f)
+    assert rowwise(got, ref) <= TOL["bf16"]
+
+
+def test_shard_partials_sum_to_full_layer_on_gpu():
+    rng = np.random.default_rng(43)
+    F, G = 300, 3
+    x, w1, w3, w2, offsets = _ffn_case(rng, [100, 0, 31, 250], 192, F, "swiglu", "bf16")
+    parts = [_run_ffn(x, w1, w3, w2, offsets, "swiglu", "bf16", out_dtype=torch.float32, col0=g * 100, f=100)
+             for g in range(G)]
+    full = oracle.expert_ffn(x, offsets, w1, w3, w2, "swiglu")
+    assert rowwise(sum(parts), full) <= TOL["bf16"]
+
+
+def test_ffn_with_no_rows():
+    rng = np.random.default_rng(0)
+    x, w1, w3, w2, offsets = _ffn_case(rng, [0, 0, 0], 64, 64, "gelu", "bf16")
+    dt = torch.bfloat16
+    packed = moe.pack_weights(to_dev(w1, dt), to_dev(w2, dt), act="gelu")
+    y = moe.expert_ffn_shard(torch.zeros((0, 64), dtype=dt, device="cuda"), to_dev(offsets, torch.int32), packed)
+    torch.cuda.synchronize()
+    assert y.shape == (0, 64)
+
+
+# ------------------------------------------------------------------------------- combine
+
+@pytest.mark.parametrize("ydt,odt", [("bf16", "bf16"), ("f32", "f32"), ("bf16", "f32"), ("f32", "bf16")])
+@pytest.mark.parametrize("T,k,h", [(1, 1, 8), (333, 2, 768), (64, 8, 136)])
+def test_combine_parity(ydt, odt, T, k, h):
+    rng = np.random.default_rng(T * k + h)
+    y_perm = rng.standard_normal((T * k, h)).astype(np.float32)
+    if ydt == "bf16":
+        y_perm = synth.round_to_bf16(y_perm)
+    pos_of = rng.permutation(T * k).reshape(T, k).astype(np.int32)
+    w = rng.random((T, k)).astype(np.float32)
+    out = moe.combine(to_dev(y_perm, tdt(ydt)), to_dev(pos_of, torch.int32), to_dev(w, torch.float32),
+                      out_dtype=tdt(odt))
+    torch.cuda.synchronize()
+    ref = oracle.combine(y_perm, pos_of, w)
+    tol = TOL["bf16"] if "bf16" in (odt,) else TOL["f32"]
+    assert rowwise(np_of(out), ref) <= tol
+
+
+# ------------------------------------------------------------------------------- whole layer
+
+def _gpu_layer(L, partial_dtype=None):
+    cfg = L.cfg
+    dt = tdt(cfg.dtype)
+    packed = moe.pack_weights(to_dev(L.w1, dt), to_dev(L.w2, dt), to_dev(L.w3, dt), act=cfg.act)
+    layer = moe.MoEShardLayer(to_dev(L.wg, dt), packed, cfg.k, bool(cfg.renorm), max_tokens=cfg.T,
+                              partial_dtype=partial_dtype)
+    x = to_dev(L.x, dt)
+    bias = to_dev(L.sel_bias, torch.float32)
+    y = layer(x, bias)
+    torch.cuda.synchronize()
+    return layer, x, bias, y
+
+
+SMALL = [("c1", None), ("c2", 1536), ("c3", 4096), ("c4", 160), ("c5", 600), ("c5dec", None)]
+
+
+@pytest.mark.parametrize("name,T", SMALL)
+def test_layer_end_to_end(name, T):
+    L = synth.make(name, seed=0, **({"T": T} if T else {}))
+    cfg = L.cfg
+    layer, x, bias, y = _gpu_layer(L)
+    ref = oracle.forward(L)
+    last = layer.last
+    gi = last["idx"].cpu().numpy()
+    same_set, order_ok = compare_routing(gi, last["w"].cpu().numpy(), ref["idx"], ref["w"], L.x, L.wg, L.sel_bias,
+                                         ref["logits"], cfg.k, cfg.dtype == "bf16")
+    tol = TOL[cfg.dtype]
+    d = last["dispatch"]
+    if same_set.all():
+        # same pick sets: grouping is unique (order inside a token does not move rows)
+        for key in ("counts", "offsets", "row_src"):
+            assert np.array_equal(getattr(d, key).cpu().numpy(), ref[key]), key
+        assert np.array_equal(by_expert(d.pos_of.cpu().numpy(), gi), by_expert(ref["pos_of"], ref["idx"]))
+        assert np.array_equal(np_of(d.x_perm), ref["x_perm"])
+        assert rowwise(np_of(last["y_perm"]), ref["y_perm"]) <= tol
+    else:
+        print(f"{name}: {(~same_set).sum()} tokens picked a different but equally valid set")
+    assert rowwise(np_of(y)[same_set], ref["y"][same_set]) <= tol
+
+
+FULL = ["c1", "c2", "c3", "c4", "c5", "c3u", "c5u"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_layer_full_size_sampled(name):
+    """Full-size workload in the benchmark's launch configuration: routing and dispatch in
+    full, outputs on sampled tokens computed one by one by the oracle."""
+    L = synth.make(name, seed=0)
+    layer, x, bias, y = _gpu_layer(L)
+    cfg = L.cfg
+    oi, ow, logits = oracle.route(L.x, L.wg, cfg.k, L.sel_bias, cfg.renorm)
+    gi = layer.last["idx"].cpu().numpy()
+    same_set, _ = compare_routing(gi, layer.last["w"].cpu().numpy(), oi, ow, L.x, L.wg, L.sel_bias, logits, cfg.k,
+                                  cfg.dtype == "bf16")
+    if same_set.all():
+        counts, offsets, row_src, pos_of = oracle.dispatch(oi, cfg.E)
+        d = layer.last["dispatch"]
+        assert np.array_equal(d.offsets.cpu().numpy(), offsets)
+        assert np.array_equal(d.row_src.cpu().numpy(), row_src)
+        assert np.array_equal(by_expert(d.pos_of.cpu().numpy(), gi), by_expert(pos_of, oi))
+    rng = np.random.default_rng(99)
+    cand = np.nonzero(same_set)[0]
+    toks = np.unique(np.concatenate([rng.choice(cand, 48, replace=False), cand[[0, -1]]]))
+    ref = oracle.layer_tokens(toks, L.x, oi, ow, L.w1, L.w3, L.w2, cfg.act)
+    assert rowwise(np_of(y)[toks], ref) <= TOL[cfg.dtype]
+
+
+def test_layer_is_deterministic():
+    L = synth.make("c5", seed=0, T=3000)
+    layer, x, bias, y1 = _gpu_layer(L)
+    y1 = y1.clone()
+    y2 = layer(x, bias)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+
+
+def test_layer_with_no_tokens():
+    L = synth.make("c2", seed=0, T=8, E=8)
+    dt = torch.bfloat16
+    packed = moe.pack_weights(to_dev(L.w1, dt), to_dev(L.w2, dt), act="gelu")
+    layer = moe.MoEShardLayer(to_dev(L.wg, dt), packed, 1, max_tokens=8)
+    y = layer(torch.zeros((0, L.cfg.h), dtype=dt, device="cuda"))
+    torch.cuda.synchronize()
+    assert y.shape == (0, L.cfg.h)
+    assert layer.last["dispatch"].counts.sum().item() == 0
