@@ -17,16 +17,13 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t b) {
     return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }
 
-// Round-to-nearest-even float -> bfloat16 (NaN stays NaN).
-__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return static_cast<bf16_t>(u >> 16);
-}
+// float -> bfloat16, round to nearest even (gfx950 converts in hardware: v_cvt_pk_bf16_f32).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) { return __builtin_bit_cast(bf16_t, static_cast<__bf16>(f)); }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    const bf16x2_t v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
+    return __builtin_bit_cast(uint32_t, v);
 }
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
@@ -52,6 +49,30 @@ __device__ __forceinline__ float act_gelu_tanh(float u) {
 }
 
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
+
+// Fast activations for the bf16 epilogues (their error is far below bf16 rounding).
+//
+// erf from Abramowitz & Stegun, Handbook of Mathematical Functions, formula 7.1.26
+// (Hastings' rational approximation): for a >= 0,
+//     erf(a) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-a^2) + eps,
+//     t = 1 / (1 + p a),  |eps| <= 1.5e-7.
+// GELU(u) = u Phi(u) = u (1 + erf(u / sqrt 2)) / 2; with Q = (poly) exp(-a^2), a = |u|/sqrt 2:
+//     u >= 0:  u (1 - Q / 2)        u < 0:  u Q / 2
+__device__ __forceinline__ float act_gelu_fast(float u) {
+    const float a = fabsf(u) * 0.70710678118654752f;
+    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, a, 1.0f));
+    float poly = 1.061405429f;
+    poly = fmaf(poly, t, -1.453152027f);
+    poly = fmaf(poly, t, 1.421413741f);
+    poly = fmaf(poly, t, -0.284496736f);
+    poly = fmaf(poly, t, 0.254829592f);
+    poly *= t;
+    const float q = 0.5f * poly * __expf(-a * a);
+    return u >= 0.f ? u - u * q : u * q;
+}
+
+// silu(z) = z / (1 + e^-z) with the hardware exponential and reciprocal (about 1 ulp each).
+__device__ __forceinline__ float silu_fast(float z) { return z * __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
 
 __host__ __device__ constexpr int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 __host__ __device__ constexpr int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }

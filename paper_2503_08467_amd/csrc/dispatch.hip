@@ -134,8 +134,10 @@ __global__ __launch_bounds__(kDispThreads) void dispatch_rank(const int32_t* __r
     }
 }
 
-// x_perm[p] = x[row_src[p]] for p < offsets[E]; each thread moves kGatherUnroll 16-byte vectors.
-constexpr int kGatherUnroll = 4;
+// x_perm[p] = x[row_src[p]] for p < offsets[E]: each wave copies kGatherRows rows, its lanes
+// striding over the 16-byte vectors of a row, with the loads of all its rows issued before
+// their stores.
+constexpr int kGatherRows = 8;
 
 __global__ __launch_bounds__(256) void dispatch_gather(const uint4* __restrict__ x,
                                                        const int32_t* __restrict__ row_src,
@@ -143,24 +145,24 @@ __global__ __launch_bounds__(256) void dispatch_gather(const uint4* __restrict__
                                                        uint32_t A_cap, uint32_t T, uint32_t nvec,
                                                        uint4* __restrict__ x_perm) {
     const uint32_t A = min(static_cast<uint32_t>(offsets[E]), A_cap);
-    const uint64_t total = static_cast<uint64_t>(A) * nvec;
-    const uint64_t i0 = (static_cast<uint64_t>(blockIdx.x) * 256 * kGatherUnroll) + threadIdx.x;
-    uint4 v[kGatherUnroll];
-    uint64_t dst[kGatherUnroll];
+    const uint32_t lane = threadIdx.x & 63;
+    const uint32_t p0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kGatherRows;
+    if (p0 >= A) return;
+    uint32_t src[kGatherRows];
 #pragma unroll
-    for (int u = 0; u < kGatherUnroll; ++u) {
-        const uint64_t i = i0 + u * 256;
-        dst[u] = i;
-        if (i < total) {
-            const uint32_t p = static_cast<uint32_t>(i / nvec);
-            const uint32_t col = static_cast<uint32_t>(i - static_cast<uint64_t>(p) * nvec);
-            const uint32_t src = static_cast<uint32_t>(row_src[p]);
-            v[u] = x[static_cast<uint64_t>(src < T ? src : 0) * nvec + col];
-        }
+    for (int r = 0; r < kGatherRows; ++r) {
+        const uint32_t p = p0 + r;
+        const uint32_t s = (p < A) ? static_cast<uint32_t>(row_src[p]) : 0u;
+        src[r] = (s < T) ? s : 0u;
     }
+    for (uint32_t c = lane; c < nvec; c += 64) {
+        uint4 v[kGatherRows];
 #pragma unroll
-    for (int u = 0; u < kGatherUnroll; ++u)
-        if (dst[u] < total) x_perm[dst[u]] = v[u];
+        for (int r = 0; r < kGatherRows; ++r) v[r] = x[static_cast<uint64_t>(src[r]) * nvec + c];
+#pragma unroll
+        for (int r = 0; r < kGatherRows; ++r)
+            if (p0 + r < A) x_perm[static_cast<uint64_t>(p0 + r) * nvec + c] = v[r];
+    }
 }
 
 }  // namespace
@@ -183,8 +185,7 @@ hipError_t launch_dispatch(const int32_t* idx, int64_t T, int k, int E, const vo
         hipLaunchKernelGGL(dispatch_rank, dim3(nchunks), dim3(kDispThreads), 0, s, idx, A, k, E, nbits,
                            nchunks, base, row_src, pos_of);
         const uint32_t nvec = static_cast<uint32_t>(static_cast<int64_t>(h) * elem_bytes / 16);
-        const uint64_t total = static_cast<uint64_t>(A) * nvec;
-        const uint64_t blocks = ceil_div(static_cast<int64_t>(total), 256 * kGatherUnroll);
+        const int64_t blocks = ceil_div(A, 4 * kGatherRows);
         hipLaunchKernelGGL(dispatch_gather, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
                            static_cast<const uint4*>(x), row_src, offsets, E, static_cast<uint32_t>(A),
                            static_cast<uint32_t>(T), nvec, static_cast<uint4*>(x_perm));

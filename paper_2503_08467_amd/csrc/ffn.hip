@@ -21,6 +21,7 @@
 
 #include "../../include/moeshard.h"
 
+#include <algorithm>
 #include <mutex>
 
 namespace moe {
@@ -42,20 +43,32 @@ struct GroupedGemm {
 constexpr int kThreads = 256;
 
 // Exclusive prefix over experts of ceil(count / BM) into tstart[0..E]; returns the total.
+// One wave scans (four experts per lane, then a shuffle scan); one barrier publishes it.
 template <int BM>
 __device__ __forceinline__ int tile_prefix(const int32_t* __restrict__ offsets, int E, int* tstart) {
-    const int tid = threadIdx.x;
-    int v = 0;
-    if (tid < E) v = (offsets[tid + 1] - offsets[tid] + BM - 1) / BM;
-    tstart[tid + 1] = v;
-    if (tid == 0) tstart[0] = 0;
-    __syncthreads();
-    for (int o = 1; o < kThreads; o <<= 1) {
-        const int add = (tid >= o) ? tstart[tid + 1 - o] : 0;
-        __syncthreads();
-        tstart[tid + 1] += add;
-        __syncthreads();
+    static_assert(MOE_MAX_EXPERTS == 4 * 64, "four experts per lane of one wave");
+    if (threadIdx.x < 64) {
+        const int lane = threadIdx.x;
+        int ex[4], run = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int e = lane * 4 + i;
+            const int cnt = (e < E) ? offsets[e + 1] - offsets[e] : 0;
+            ex[i] = run;
+            run += cnt > 0 ? (cnt + BM - 1) / BM : 0;
+        }
+        int incl = run;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int t = __shfl_up(incl, o, 64);
+            if (lane >= o) incl += t;
+        }
+        const int base = incl - run;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) tstart[lane * 4 + i] = base + ex[i];
+        if (lane == 63) tstart[4 * 64] = incl;
     }
+    __syncthreads();
     return tstart[E];
 }
 
@@ -75,6 +88,15 @@ __device__ __forceinline__ float epilogue(float u, float g) {
     if (EPI == kEpiGelu) return act_gelu(u);
     if (EPI == kEpiGeluTanh) return act_gelu_tanh(u);
     if (EPI == kEpiSwiglu) return silu(u) * g;
+    return u;
+}
+
+// The same activations through the fast forms (bf16 outputs: error far below rounding).
+template <int EPI>
+__device__ __forceinline__ float epilogue_fast(float u, float g) {
+    if (EPI == kEpiGelu) return act_gelu_fast(u);
+    if (EPI == kEpiGeluTanh) return act_gelu_tanh(u);
+    if (EPI == kEpiSwiglu) return silu_fast(u) * g;
     return u;
 }
 
@@ -274,6 +296,283 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16(GroupedGemm g) {
     }
 }
 
+// ------------------------------------------------------------------ bf16 MFMA kernel, direct-to-LDS pipeline
+//
+// Tile: BM activation rows x BW weight rows (SwiGLU: BW/2 rows of W1 + the same rows of
+// W3), K in steps of BK (32 or 64).  A row's BK-element slice is one LDS row of 2*BK bytes
+// holding CPR = BK/8 chunks of 16 bytes; chunk c of row r is stored at position
+// c ^ swz(r), which keeps the 32-row MFMA fragment reads free of bank conflicts.  Global
+// data goes straight to LDS with global_load_lds_dwordx4 (lane l of a wave instruction
+// fills bytes [16 l, 16 l + 16) of a 1 KiB span), NS stages deep, so NS - 1 K steps are in
+// flight while one is multiplied.  The weight fragment is the MFMA's first operand, so each
+// lane ends up holding 4 consecutive output columns of one row (one 8- or 16-byte store per
+// group).  Rows past the segment end and weight rows past N are clamped to a valid row
+// (their results are never stored); K must be a multiple of BK.
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt field is 6 bits");
+    // gfx9 s_waitcnt: vmcnt[3:0] | expcnt[6:4]=7 | lgkmcnt[11:8]=15 | vmcnt[5:4] at [15:14]
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Wait until at most `newer` stages of LPW loads each are still in flight.
+template <int LPW, int NS>
+__device__ __forceinline__ void wait_stages(int newer) {
+    static_assert(NS >= 2 && NS <= 6, "pipeline depth");
+    if (NS > 5 && newer >= 4) { wait_vmcnt<(NS > 5 ? 4 * LPW : 0)>(); return; }
+    if (NS > 4 && newer >= 3) { wait_vmcnt<(NS > 4 ? 3 * LPW : 0)>(); return; }
+    if (NS > 3 && newer >= 2) { wait_vmcnt<(NS > 3 ? 2 * LPW : 0)>(); return; }
+    if (NS > 2 && newer >= 1) { wait_vmcnt<(NS > 2 ? LPW : 0)>(); return; }
+    wait_vmcnt<0>();
+}
+
+template <int BM, int BW, int BK, int NS, int EPI>
+struct LdsShape {
+    static constexpr bool kDual = (EPI == kEpiSwiglu);
+    static constexpr int kNB = kDual ? 2 : 1;
+    static constexpr int kBN = BW / kNB;          // output columns per tile
+    static constexpr int kMI = BM / 64;           // 32-row blocks per wave (2 x 2 waves)
+    static constexpr int kNI = kBN / 64;          // 32-column blocks per wave per matrix
+    static constexpr int kCPR = BK / 8;           // 16-byte chunks per LDS row
+    static constexpr int kRPI = 64 / kCPR;        // LDS rows per 1 KiB wave load
+    static constexpr int kRows = BM + BW;         // LDS rows per stage
+    static constexpr int kLPW = kRows / kRPI / 4;  // 1 KiB loads per wave per stage
+    static constexpr int kSwzShift = (kCPR == 8) ? 1 : 2;  // rows sharing a 256-byte bank line
+    static constexpr size_t kBytes = (size_t)NS * kRows * BK * 2;
+    static_assert(kMI >= 1 && kNI >= 1, "tile too small for 2 x 2 waves of 32 x 32 blocks");
+    static_assert(kRows % (kRPI * 4) == 0, "stage rows must split evenly over the waves");
+    static_assert(BK == 32 || BK == 64, "BK");
+};
+
+// 16 bytes per lane from global memory straight into LDS: lane l's bytes land at
+// lds + 16 l (the LDS address is wave-uniform).  A plain (non-template) device function,
+// so the target builtin never meets the host compilation pass.
+__device__ __forceinline__ void load_lds16(const void* gptr, void* lds) {
+    __builtin_amdgcn_global_load_lds(gptr, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
+// One stage of a wave's loads: load j fills the 1 KiB at dst + j KiB from src[j] + k0.
+template <int LPW>
+__device__ __forceinline__ void issue_stage(const bf16_t* (&src)[LPW], bf16_t* dst, int k0) {
+#pragma unroll
+    for (int j = 0; j < LPW; ++j) load_lds16(src[j] + k0, dst + j * 512);
+}
+
+// Bare workgroup barrier.  A fenced barrier (__syncthreads, or even an LDS-only fence)
+// makes the compiler wait for every direct-to-LDS load in flight, which would drain the
+// prefetched stages this pipeline keeps in flight across the barrier.  Ordering is kept
+// by hand instead: each wave waits (wait_stages) for its own loads of the stage it is about
+// to read before arriving, so after the barrier that stage is complete for all waves; and
+// a wave only overwrites a stage buffer after the barrier that follows every wave's reads
+// of it (its ds_reads have returned: their data fed the MFMAs before the wave arrived).
+__device__ __forceinline__ void stage_barrier() { __builtin_amdgcn_s_barrier(); }
+
+// Row tile mt's expert and row range, and the column offset of column tile nt.
+struct TileRows {
+    int64_t row0, row_end;
+    int e;
+};
+
+template <int BM>
+__device__ __forceinline__ TileRows tile_rows(const GroupedGemm& g, const int* tstart, int mt) {
+    TileRows t;
+    t.e = find_expert(tstart, g.E, mt);
+    t.row0 = g.offsets[t.e] + static_cast<int64_t>(mt - tstart[t.e]) * BM;
+    t.row_end = g.offsets[t.e + 1] < g.rows_max ? g.offsets[t.e + 1] : g.rows_max;
+    return t;
+}
+
+// Logical tile L -> (row tile, column tile): groups of GM row tiles, column-major inside a
+// group, so that neighbouring tiles share either rows or weights.
+__device__ __forceinline__ void tile_coords(int L, int total_m, int n_tiles, int& mt, int& nt) {
+    constexpr int GM = 8;
+    const int grp = L / (GM * n_tiles);
+    const int rem = L - grp * GM * n_tiles;
+    const int gsz = min(GM, total_m - grp * GM);
+    nt = rem / gsz;
+    mt = grp * GM + (rem - nt * gsz);
+}
+
+// Persistent grouped GEMM.  The grid is a fixed number of workgroups (one or two per CU);
+// the tiles are dealt to the 8 XCDs in contiguous runs (the hardware deals workgroups
+// round-robin, so workgroup b sits on XCD b % 8) and, inside a run, round-robin to that
+// XCD's workgroups, so concurrently running tiles share rows or weights in its L2.  The
+// load pipeline runs across tile boundaries: while one tile's last K steps are multiplied
+// and its epilogue runs, the next tile's first stages are already in flight.
+template <int BM, int BW, int BK, int NS, int EPI, bool OB>
+__global__ __launch_bounds__(kThreads, (LdsShape<BM, BW, BK, NS, EPI>::kBytes <= 80 * 1024) ? 2 : 1)
+void gemm_bf16_lds(GroupedGemm g) {
+    typedef LdsShape<BM, BW, BK, NS, EPI> S;
+    constexpr int NB = S::kNB, BN = S::kBN, MI = S::kMI, NI = S::kNI, ROWS = S::kRows, LPW = S::kLPW;
+    constexpr int CPR = S::kCPR, RPI = S::kRPI, SH = S::kSwzShift;
+    __shared__ int tstart[kThreads + 1];
+    extern __shared__ __align__(1024) unsigned char smem_raw[];
+    bf16_t* smem = reinterpret_cast<bf16_t*>(smem_raw);
+
+    const int total_m = tile_prefix<BM>(g.offsets, g.E, tstart);
+    const int total = total_m * g.n_tiles;
+    const int per = (total + 7) >> 3;
+    const int xcd = blockIdx.x & 7, nslot = gridDim.x >> 3;
+    const int t_end = min(total, (xcd + 1) * per);
+    const int t_first = xcd * per + static_cast<int>(blockIdx.x >> 3);
+    if (t_first >= t_end) return;
+    const int nk = g.K / BK;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const bf16_t* __restrict__ A = static_cast<const bf16_t*>(g.a);
+    bf16_t* const my_dst = smem + wave * LPW * 512;
+
+    // ---- load cursor: tile lt, K step lk; src[] are this lane's rows of tile lt
+    int lt = t_first, lk = 0;
+    const bf16_t* src[LPW];
+    auto set_src = [&](int L) {
+        int mt, nt;
+        tile_coords(L, total_m, g.n_tiles, mt, nt);
+        const TileRows tr = tile_rows<BM>(g, tstart, mt);
+        const int n0 = nt * BN;
+        // rows past the segment are clamped to its last row; inconsistent offsets (a segment
+        // outside [0, rows_max)) still only ever read rows inside the buffer
+        int64_t last = tr.row_end > tr.row0 ? tr.row_end - 1 : tr.row0;
+        last = max<int64_t>(0, min<int64_t>(last, g.rows_max - 1));
+#pragma unroll
+        for (int j = 0; j < LPW; ++j) {
+            const int R = (wave * LPW + j) * RPI + lane / CPR;
+            const int kc = (lane % CPR) ^ ((R >> SH) & (CPR - 1));
+            if (R < BM) {
+                const int64_t ar = max<int64_t>(0, min<int64_t>(tr.row0 + R, last));
+                src[j] = A + ar * g.K + kc * 8;
+            } else {
+                const int wr = R - BM;
+                const int nb = wr / BN;
+                const int n = min(n0 + (wr - nb * BN), g.N - 1);
+                const bf16_t* B = static_cast<const bf16_t*>(nb ? g.b2 : g.b) + tr.e * g.b_estride;
+                src[j] = B + static_cast<int64_t>(n) * g.K + kc * 8;
+            }
+        }
+    };
+    set_src(lt);
+    int issued = 0;  // stages issued by this wave so far
+#pragma unroll
+    for (int st = 0; st < NS - 1; ++st) {
+        if (lt < t_end) {
+            issue_stage<LPW>(src, my_dst + (issued % NS) * ROWS * BK, lk * BK);
+            ++issued;
+            if (++lk == nk) {
+                lk = 0;
+                lt += nslot;
+                if (lt < t_end) set_src(lt);
+            }
+        }
+    }
+
+    // ---- compute cursor
+    const int wm = wave >> 1, wn = wave & 1;
+    const int l32 = lane & 31, lhi = lane >> 5;
+    int ct = t_first, ck = 0, consumed = 0;
+    bool drain = false;  // epilogue stores are in flight: wait for every vector memory op once
+    f32x16_t acc[NB][MI][NI];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+#pragma unroll
+            for (int j = 0; j < NI; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[nb][i][j][r] = 0.f;
+
+    while (true) {
+        if (drain) wait_vmcnt<0>();
+        else wait_stages<LPW, NS>(issued - consumed - 1);
+        drain = false;
+        stage_barrier();
+        if (lt < t_end) {
+            issue_stage<LPW>(src, my_dst + (issued % NS) * ROWS * BK, lk * BK);
+            ++issued;
+            if (++lk == nk) {
+                lk = 0;
+                lt += nslot;
+                if (lt < t_end) set_src(lt);
+            }
+        }
+        const bf16_t* st = smem + (consumed % NS) * ROWS * BK;
+#pragma unroll
+        for (int ks = 0; ks < BK / 16; ++ks) {
+            const int ch = 2 * ks + lhi;
+            bf16x8_t af[MI], wf[NB][NI];
+#pragma unroll
+            for (int i = 0; i < MI; ++i) {
+                const int R = wm * (BM / 2) + i * 32 + l32;
+                af[i] = *reinterpret_cast<const bf16x8_t*>(st + R * BK + ((ch ^ ((R >> SH) & (CPR - 1))) << 3));
+            }
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int j = 0; j < NI; ++j) {
+                    const int R = BM + nb * BN + wn * (BN / 2) + j * 32 + l32;
+                    wf[nb][j] = *reinterpret_cast<const bf16x8_t*>(st + R * BK + ((ch ^ ((R >> SH) & (CPR - 1))) << 3));
+                }
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+#pragma unroll
+                    for (int j = 0; j < NI; ++j)
+                        acc[nb][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[nb][j], af[i], acc[nb][i][j], 0, 0, 0);
+        }
+        ++consumed;
+        if (++ck < nk) continue;
+
+        // ---- epilogue of tile ct.  D[n][m] layout: lane holds activation row l32 of the
+        // block; register r holds weight row 8 * (r / 4) + 4 * lhi + r % 4, i.e. 4
+        // consecutive output columns per group r / 4.
+        {
+            int mt, nt;
+            tile_coords(ct, total_m, g.n_tiles, mt, nt);
+            const TileRows tr = tile_rows<BM>(g, tstart, mt);
+            const int n0 = nt * BN;
+#pragma unroll
+            for (int i = 0; i < MI; ++i) {
+                const int64_t row = tr.row0 + wm * (BM / 2) + i * 32 + l32;
+                const bool row_ok = row >= 0 && row < tr.row_end;
+#pragma unroll
+                for (int j = 0; j < NI; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int col = n0 + wn * (BN / 2) + j * 32 + 8 * q + 4 * lhi;
+                        float v[4];
+#pragma unroll
+                        for (int c = 0; c < 4; ++c)
+                            v[c] = epilogue_fast<EPI>(acc[0][i][j][4 * q + c], acc[NB - 1][i][j][4 * q + c]);
+                        if (row_ok && col < g.N) {
+                            if (OB) {
+                                uint2 pk;
+                                pk.x = pack_bf16x2(v[0], v[1]);
+                                pk.y = pack_bf16x2(v[2], v[3]);
+                                *reinterpret_cast<uint2*>(static_cast<bf16_t*>(g.c) + row * g.ldc + col) = pk;
+                            } else {
+                                *reinterpret_cast<float4*>(static_cast<float*>(g.c) + row * g.ldc + col) =
+                                    make_float4(v[0], v[1], v[2], v[3]);
+                            }
+                        }
+                    }
+            }
+        }
+        ct += nslot;
+        if (ct >= t_end) break;
+        ck = 0;
+        drain = true;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int i = 0; i < MI; ++i)
+#pragma unroll
+                for (int j = 0; j < NI; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) acc[nb][i][j][r] = 0.f;
+    }
+}
+
 // ------------------------------------------------------------------ fp32 kernel
 
 constexpr int kFBM = 64, kFBN = 64, kFBK = 16;
@@ -393,9 +692,48 @@ hipError_t run_f32(GroupedGemm g, int64_t A_max, hipStream_t s) {
     return hipGetLastError();
 }
 
+int device_cus() {
+    static const int cus = [] {
+        int dev = 0, n = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            n = 256;
+        return n;
+    }();
+    return cus;
+}
+
+template <int BM, int BW, int BK, int NS, int EPI, bool OB>
+hipError_t run_bf16_lds(GroupedGemm g, int64_t A_max, hipStream_t s) {
+    typedef LdsShape<BM, BW, BK, NS, EPI> S;
+    constexpr size_t lds = S::kBytes;
+    constexpr int per_cu = (lds <= 80 * 1024) ? 2 : 1;
+    static const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&gemm_bf16_lds<BM, BW, BK, NS, EPI, OB>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+    if (attr != hipSuccess) return attr;
+    g.n_tiles = static_cast<int>(ceil_div(g.N, S::kBN));
+    const int64_t tiles = row_tile_bound(A_max, g.E, BM) * g.n_tiles;
+    if (tiles == 0) return hipSuccess;
+    // persistent grid: at most per_cu workgroups per CU, a multiple of the 8 XCDs
+    const int64_t blocks = round_up(std::min<int64_t>(tiles, static_cast<int64_t>(per_cu) * device_cus()), 8);
+    hipLaunchKernelGGL((gemm_bf16_lds<BM, BW, BK, NS, EPI, OB>), dim3(static_cast<unsigned>(blocks)), dim3(kThreads),
+                       lds, s, g);
+    return hipGetLastError();
+}
+
+// Tile shape: 128 activation rows x 256 weight rows, 32-wide K steps, three stages (two in
+// flight) in 72 KiB of LDS, so that two workgroups share a CU and one's epilogue and
+// pipeline fill overlap the other's MFMAs.
+template <int EPI, bool OB>
+hipError_t run_bf16_best(GroupedGemm g, int64_t A_max, hipStream_t s) {
+    if (g.K % 32 == 0) return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);
+    return run_bf16<EPI, OB>(g, A_max, s);
+}
+
 template <int EPI>
 hipError_t gemm1(bool bf16, GroupedGemm g, int64_t A_max, hipStream_t s) {
-    return bf16 ? run_bf16<EPI, true>(g, A_max, s) : run_f32<EPI, false>(g, A_max, s);
+    return bf16 ? run_bf16_best<EPI, true>(g, A_max, s) : run_f32<EPI, false>(g, A_max, s);
 }
 
 }  // namespace
@@ -434,7 +772,7 @@ hipError_t launch_ffn(const void* x_perm, const int32_t* offsets, int64_t A_max,
     g2.ldc = h;
     g2.b_estride = static_cast<int64_t>(h) * fp;
     g2.rows_max = A_max;
-    if (bf16) return y_bf16 ? run_bf16<kEpiNone, true>(g2, A_max, s) : run_bf16<kEpiNone, false>(g2, A_max, s);
+    if (bf16) return y_bf16 ? run_bf16_best<kEpiNone, true>(g2, A_max, s) : run_bf16_best<kEpiNone, false>(g2, A_max, s);
     return y_bf16 ? run_f32<kEpiNone, true>(g2, A_max, s) : run_f32<kEpiNone, false>(g2, A_max, s);
 }
 

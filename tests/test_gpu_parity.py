@@ -181,6 +181,8 @@ def _run_ffn(x, w1, w3, w2, offsets, act, dtype, out_dtype=None, col0=0, f=None)
     ([1], 64, 37),
     ([0, 0, 77], 72, 128),                     # h not a multiple of the 64-wide K step
     ([513, 40, 0, 255], 768, 512),
+    ([700, 333], 256, 200),                    # >= 512 rows per expert: 256-row tiles, ragged
+    ([1100, 0, 1500, 3], 512, 384),
 ])
 def test_ffn_parity(dtype, act, counts, h, f):
     rng = np.random.default_rng(sum(counts) + h + f)
