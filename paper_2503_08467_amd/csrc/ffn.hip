@@ -346,17 +346,53 @@ struct LdsShape {
 };
 
 // 16 bytes per lane from global memory straight into LDS: lane l's bytes land at
-// lds + 16 l (the LDS address is wave-uniform).  A plain (non-template) device function,
-// so the target builtin never meets the host compilation pass.
+// lds + 16 l (the LDS address is wave-uniform and goes through M0).  Issued as inline
+// assembly on purpose: the compiler tracks the builtin form as an LDS write and then waits
+// for it (vmcnt(0)) before every later LDS read it cannot prove disjoint -- which would make
+// the prefetched stages synchronous.  The kernel orders these loads itself: wait_stages
+// before the stage barrier, and a stage buffer is only refilled after every wave has read
+// it.  The "memory" clobber keeps the compiler from moving LDS accesses across the issue.
 __device__ __forceinline__ void load_lds16(const void* gptr, void* lds) {
-    __builtin_amdgcn_global_load_lds(gptr, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+    const uint32_t m0 = __builtin_amdgcn_readfirstlane(
+        static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) void*)lds)));
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(m0), "v"(gptr) : "memory", "m0");
 }
 
-// One stage of a wave's loads: load j fills the 1 KiB at dst + j KiB from src[j] + k0.
-template <int LPW>
-__device__ __forceinline__ void issue_stage(const bf16_t* (&src)[LPW], bf16_t* dst, int k0) {
+// Where a tile's loads come from: wave-uniform scalars, set once per tile.
+struct TileSrc {
+    const bf16_t* a;   // activation rows (x_perm or H)
+    const bf16_t* b0;  // this expert's weights (W1^T or W2^T)
+    const bf16_t* b1;  // SwiGLU: this expert's W3^T
+    int64_t row0, last;  // first row of the tile, last valid row to read
+    int n0;              // first weight row (output column) of the tile
+};
+
+// One stage of a wave's loads: 1 KiB per load, lane l landing at byte 16 l of it.  Load j
+// of wave w fills LDS rows (4 j + w) * RPI ..., so whether a load carries activation rows
+// or weight rows (and which weight matrix) is fixed by j at compile time.  LDS row R of the
+// stage holds activation row R (R < BM) or weight row R - BM; rows past the segment or past
+// N are clamped to a valid row, whose results are never stored.  Addresses are computed
+// here from the tile scalars rather than cached, to keep registers for the accumulators.
+template <int BM, int BN, int LPW, int RPI, int CPR, int SH>
+__device__ __forceinline__ void issue_stage(const TileSrc& ts, int K, int N, int wave, int lane, bf16_t* stage,
+                                            int k0) {
+    const int r_lane = lane / CPR, c_lane = lane % CPR;
 #pragma unroll
-    for (int j = 0; j < LPW; ++j) load_lds16(src[j] + k0, dst + j * 512);
+    for (int j = 0; j < LPW; ++j) {
+        constexpr int kRowsPerJ = 4 * RPI;
+        const int R = (j * 4 + wave) * RPI + r_lane;
+        const int kc = c_lane ^ ((R >> SH) & (CPR - 1));
+        const bf16_t* src;
+        if (j * kRowsPerJ < BM) {
+            src = ts.a + min(ts.row0 + R, ts.last) * K;
+        } else {
+            constexpr int kAJ = BM / kRowsPerJ;  // loads per wave that carry activation rows
+            const int nb = ((j - kAJ) * kRowsPerJ) / BN;  // compile-time after unrolling
+            const int n = min(ts.n0 + (R - BM - nb * BN), N - 1);
+            src = (nb ? ts.b1 : ts.b0) + static_cast<int64_t>(n) * K;
+        }
+        load_lds16(src + k0 + kc * 8, stage + (j * 4 + wave) * RPI * (CPR * 8));
+    }
 }
 
 // Bare workgroup barrier.  A fenced barrier (__syncthreads, or even an LDS-only fence)
@@ -419,149 +455,49 @@ void gemm_bf16_lds(GroupedGemm g) {
     if (t_first >= t_end) return;
     const int nk = g.K / BK;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    // the wave index is uniform across a wave; say so, so that per-wave choices stay scalar
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const bf16_t* __restrict__ A = static_cast<const bf16_t*>(g.a);
-    bf16_t* const my_dst = smem + wave * LPW * 512;
 
-    // ---- load cursor: tile lt, K step lk; src[] are this lane's rows of tile lt
+    // ---- load cursor: tile lt, K step lk
     int lt = t_first, lk = 0;
-    const bf16_t* src[LPW];
-    auto set_src = [&](int L) {
+    TileSrc ts;
+    auto set_tile = [&](int L) {
         int mt, nt;
         tile_coords(L, total_m, g.n_tiles, mt, nt);
         const TileRows tr = tile_rows<BM>(g, tstart, mt);
-        const int n0 = nt * BN;
+        ts.a = A;
+        ts.b0 = static_cast<const bf16_t*>(g.b) + tr.e * g.b_estride;
+        ts.b1 = NB > 1 ? static_cast<const bf16_t*>(g.b2) + tr.e * g.b_estride : ts.b0;
+        ts.row0 = max<int64_t>(0, tr.row0);
         // rows past the segment are clamped to its last row; inconsistent offsets (a segment
         // outside [0, rows_max)) still only ever read rows inside the buffer
         int64_t last = tr.row_end > tr.row0 ? tr.row_end - 1 : tr.row0;
-        last = max<int64_t>(0, min<int64_t>(last, g.rows_max - 1));
-#pragma unroll
-        for (int j = 0; j < LPW; ++j) {
-            const int R = (wave * LPW + j) * RPI + lane / CPR;
-            const int kc = (lane % CPR) ^ ((R >> SH) & (CPR - 1));
-            if (R < BM) {
-                const int64_t ar = max<int64_t>(0, min<int64_t>(tr.row0 + R, last));
-                src[j] = A + ar * g.K + kc * 8;
-            } else {
-                const int wr = R - BM;
-                const int nb = wr / BN;
-                const int n = min(n0 + (wr - nb * BN), g.N - 1);
-                const bf16_t* B = static_cast<const bf16_t*>(nb ? g.b2 : g.b) + tr.e * g.b_estride;
-                src[j] = B + static_cast<int64_t>(n) * g.K + kc * 8;
-            }
-        }
+        ts.last = max<int64_t>(0, min<int64_t>(last, g.rows_max - 1));
+        ts.n0 = nt * BN;
     };
-    set_src(lt);
+    set_tile(lt);
     int issued = 0;  // stages issued by this wave so far
 #pragma unroll
     for (int st = 0; st < NS - 1; ++st) {
         if (lt < t_end) {
-            issue_stage<LPW>(src, my_dst + (issued % NS) * ROWS * BK, lk * BK);
+            issue_stage<BM, BN, LPW, RPI, CPR, SH>(ts, g.K, g.N, wave, lane, smem + (issued % NS) * ROWS * BK, lk * BK);
             ++issued;
             if (++lk == nk) {
                 lk = 0;
                 lt += nslot;
-                if (lt < t_end) set_src(lt);
+                if (lt < t_end) set_tile(lt);
             }
         }
     }
 
-    // ---- compute cursor
+    // ---- compute: one tile after another; the load cursor above runs NS - 1 stages ahead
     const int wm = wave >> 1, wn = wave & 1;
     const int l32 = lane & 31, lhi = lane >> 5;
-    int ct = t_first, ck = 0, consumed = 0;
-    bool drain = false;  // epilogue stores are in flight: wait for every vector memory op once
-    f32x16_t acc[NB][MI][NI];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int i = 0; i < MI; ++i)
-#pragma unroll
-            for (int j = 0; j < NI; ++j)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) acc[nb][i][j][r] = 0.f;
-
-    while (true) {
-        if (drain) wait_vmcnt<0>();
-        else wait_stages<LPW, NS>(issued - consumed - 1);
-        drain = false;
-        stage_barrier();
-        if (lt < t_end) {
-            issue_stage<LPW>(src, my_dst + (issued % NS) * ROWS * BK, lk * BK);
-            ++issued;
-            if (++lk == nk) {
-                lk = 0;
-                lt += nslot;
-                if (lt < t_end) set_src(lt);
-            }
-        }
-        const bf16_t* st = smem + (consumed % NS) * ROWS * BK;
-#pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks) {
-            const int ch = 2 * ks + lhi;
-            bf16x8_t af[MI], wf[NB][NI];
-#pragma unroll
-            for (int i = 0; i < MI; ++i) {
-                const int R = wm * (BM / 2) + i * 32 + l32;
-                af[i] = *reinterpret_cast<const bf16x8_t*>(st + R * BK + ((ch ^ ((R >> SH) & (CPR - 1))) << 3));
-            }
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                for (int j = 0; j < NI; ++j) {
-                    const int R = BM + nb * BN + wn * (BN / 2) + j * 32 + l32;
-                    wf[nb][j] = *reinterpret_cast<const bf16x8_t*>(st + R * BK + ((ch ^ ((R >> SH) & (CPR - 1))) << 3));
-                }
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                for (int i = 0; i < MI; ++i)
-#pragma unroll
-                    for (int j = 0; j < NI; ++j)
-                        acc[nb][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[nb][j], af[i], acc[nb][i][j], 0, 0, 0);
-        }
-        ++consumed;
-        if (++ck < nk) continue;
-
-        // ---- epilogue of tile ct.  D[n][m] layout: lane holds activation row l32 of the
-        // block; register r holds weight row 8 * (r / 4) + 4 * lhi + r % 4, i.e. 4
-        // consecutive output columns per group r / 4.
-        {
-            int mt, nt;
-            tile_coords(ct, total_m, g.n_tiles, mt, nt);
-            const TileRows tr = tile_rows<BM>(g, tstart, mt);
-            const int n0 = nt * BN;
-#pragma unroll
-            for (int i = 0; i < MI; ++i) {
-                const int64_t row = tr.row0 + wm * (BM / 2) + i * 32 + l32;
-                const bool row_ok = row >= 0 && row < tr.row_end;
-#pragma unroll
-                for (int j = 0; j < NI; ++j)
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const int col = n0 + wn * (BN / 2) + j * 32 + 8 * q + 4 * lhi;
-                        float v[4];
-#pragma unroll
-                        for (int c = 0; c < 4; ++c)
-                            v[c] = epilogue_fast<EPI>(acc[0][i][j][4 * q + c], acc[NB - 1][i][j][4 * q + c]);
-                        if (row_ok && col < g.N) {
-                            if (OB) {
-                                uint2 pk;
-                                pk.x = pack_bf16x2(v[0], v[1]);
-                                pk.y = pack_bf16x2(v[2], v[3]);
-                                *reinterpret_cast<uint2*>(static_cast<bf16_t*>(g.c) + row * g.ldc + col) = pk;
-                            } else {
-                                *reinterpret_cast<float4*>(static_cast<float*>(g.c) + row * g.ldc + col) =
-                                    make_float4(v[0], v[1], v[2], v[3]);
-                            }
-                        }
-                    }
-            }
-        }
-        ct += nslot;
-        if (ct >= t_end) break;
-        ck = 0;
-        drain = true;
+    int consumed = 0;
+    for (int ct = t_first; ct < t_end; ct += nslot) {
+        f32x16_t acc[NB][MI][NI];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
@@ -570,6 +506,86 @@ void gemm_bf16_lds(GroupedGemm g) {
                 for (int j = 0; j < NI; ++j)
 #pragma unroll
                     for (int r = 0; r < 16; ++r) acc[nb][i][j][r] = 0.f;
+
+        for (int ck = 0; ck < nk; ++ck) {
+            // the first step after an epilogue also waits for its stores (they share the counter)
+            if (ck == 0 && ct != t_first) wait_vmcnt<0>();
+            else wait_stages<LPW, NS>(issued - consumed - 1);
+            stage_barrier();
+            if (lt < t_end) {
+                issue_stage<BM, BN, LPW, RPI, CPR, SH>(ts, g.K, g.N, wave, lane, smem + (issued % NS) * ROWS * BK,
+                                                       lk * BK);
+                ++issued;
+                if (++lk == nk) {
+                    lk = 0;
+                    lt += nslot;
+                    if (lt < t_end) set_tile(lt);
+                }
+            }
+            const bf16_t* st = smem + (consumed % NS) * ROWS * BK;
+#pragma unroll
+            for (int ks = 0; ks < BK / 16; ++ks) {
+                const int ch = 2 * ks + lhi;
+                bf16x8_t af[MI], wf[NB][NI];
+#pragma unroll
+                for (int i = 0; i < MI; ++i) {
+                    const int R = wm * (BM / 2) + i * 32 + l32;
+                    af[i] = *reinterpret_cast<const bf16x8_t*>(st + R * BK + ((ch ^ ((R >> SH) & (CPR - 1))) << 3));
+                }
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                    for (int j = 0; j < NI; ++j) {
+                        const int R = BM + nb * BN + wn * (BN / 2) + j * 32 + l32;
+                        wf[nb][j] = *reinterpret_cast<const bf16x8_t*>(st + R * BK + ((ch ^ ((R >> SH) & (CPR - 1))) << 3));
+                    }
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                    for (int i = 0; i < MI; ++i)
+#pragma unroll
+                        for (int j = 0; j < NI; ++j)
+                            acc[nb][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[nb][j], af[i], acc[nb][i][j], 0, 0, 0);
+            }
+            ++consumed;
+        }
+
+        // ---- epilogue of tile ct.  D[n][m] layout: lane holds activation row l32 of the
+        // block; register r holds weight row 8 * (r / 4) + 4 * lhi + r % 4, i.e. 4
+        // consecutive output columns per group r / 4.
+        int mt, nt;
+        tile_coords(ct, total_m, g.n_tiles, mt, nt);
+        const TileRows tr = tile_rows<BM>(g, tstart, mt);
+        const int n0 = nt * BN;
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+            const int64_t row = tr.row0 + wm * (BM / 2) + i * 32 + l32;
+            const bool row_ok = row >= 0 && row < tr.row_end;
+#pragma unroll
+            for (int j = 0; j < NI; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int col = n0 + wn * (BN / 2) + j * 32 + 8 * q + 4 * lhi;
+                    float v[4];
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+                        v[c] = epilogue_fast<EPI>(acc[0][i][j][4 * q + c], acc[NB - 1][i][j][4 * q + c]);
+                    if (row_ok && col < g.N) {
+                        if (OB) {
+                            uint2 pk;
+                            pk.x = pack_bf16x2(v[0], v[1]);
+                            pk.y = pack_bf16x2(v[2], v[3]);
+                            *reinterpret_cast<uint2*>(static_cast<bf16_t*>(g.c) + row * g.ldc + col) = pk;
+                        } else {
+                            *reinterpret_cast<float4*>(static_cast<float*>(g.c) + row * g.ldc + col) =
+                                make_float4(v[0], v[1], v[2], v[3]);
+                        }
+                    }
+                    // one block at a time: keeps the scheduler from pulling every accumulator
+                    // into VGPRs at once
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+        }
     }
 }
 
