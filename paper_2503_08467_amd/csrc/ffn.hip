@@ -303,11 +303,10 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16(GroupedGemm g) {
 // holding CPR = BK/8 chunks of 16 bytes; chunk c of row r is stored at position
 // c ^ swz(r), which keeps the 32-row MFMA fragment reads free of bank conflicts.  Global
 // data goes straight to LDS with global_load_lds_dwordx4 (lane l of a wave instruction
-// fills bytes [16 l, 16 l + 16) of a 1 KiB span), NS stages deep, so NS - 1 K steps are in
-// flight while one is multiplied.  The weight fragment is the MFMA's first operand, so each
-// lane ends up holding 4 consecutive output columns of one row (one 8- or 16-byte store per
-// group).  Rows past the segment end and weight rows past N are clamped to a valid row
-// (their results are never stored); K must be a multiple of BK.
+// fills bytes [16 l, 16 l + 16) of a 1 KiB span), NS stages deep.  The weight fragment is
+// the MFMA's first operand, so each lane ends up holding 4 consecutive output columns of
+// one row (one 8- or 16-byte store per group).  K must be a multiple of BK and N (per
+// weight matrix) a multiple of the tile's columns, or at most one tile wide.
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -315,6 +314,8 @@ __device__ __forceinline__ void wait_vmcnt() {
     // gfx9 s_waitcnt: vmcnt[3:0] | expcnt[6:4]=7 | lgkmcnt[11:8]=15 | vmcnt[5:4] at [15:14]
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
+
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (0 << 8) | (3 << 14)); }
 
 // Wait until at most `newer` stages of LPW loads each are still in flight.
 template <int LPW, int NS>
@@ -338,73 +339,77 @@ struct LdsShape {
     static constexpr int kRPI = 64 / kCPR;        // LDS rows per 1 KiB wave load
     static constexpr int kRows = BM + BW;         // LDS rows per stage
     static constexpr int kLPW = kRows / kRPI / 4;  // 1 KiB loads per wave per stage
+    static constexpr int kKS = BK / 16;           // MFMA K steps per stage
     static constexpr int kSwzShift = (kCPR == 8) ? 1 : 2;  // rows sharing a 256-byte bank line
     static constexpr size_t kBytes = (size_t)NS * kRows * BK * 2;
+    static constexpr int kPerCU = (kBytes <= 80 * 1024) ? 2 : 1;  // workgroups per CU
     static_assert(kMI >= 1 && kNI >= 1, "tile too small for 2 x 2 waves of 32 x 32 blocks");
     static_assert(kRows % (kRPI * 4) == 0, "stage rows must split evenly over the waves");
+    static_assert(BM % (4 * kRPI) == 0 && kBN % (4 * kRPI) == 0, "a wave load carries one kind of row");
     static_assert(BK == 32 || BK == 64, "BK");
 };
 
-// 16 bytes per lane from global memory straight into LDS: lane l's bytes land at
-// lds + 16 l (the LDS address is wave-uniform and goes through M0).  Issued as inline
-// assembly on purpose: the compiler tracks the builtin form as an LDS write and then waits
-// for it (vmcnt(0)) before every later LDS read it cannot prove disjoint -- which would make
-// the prefetched stages synchronous.  The kernel orders these loads itself: wait_stages
-// before the stage barrier, and a stage buffer is only refilled after every wave has read
-// it.  The "memory" clobber keeps the compiler from moving LDS accesses across the issue.
-__device__ __forceinline__ void load_lds16(const void* gptr, void* lds) {
-    const uint32_t m0 = __builtin_amdgcn_readfirstlane(
-        static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) void*)lds)));
-    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(m0), "v"(gptr) : "memory", "m0");
+// 16 bytes per lane from global memory straight into LDS: lane l's bytes come from
+// base + voff(l) and land at lds + 16 l (the LDS address is wave-uniform and goes through
+// M0; base is a wave-uniform 64-bit address in scalar registers, voff a 32-bit per-lane
+// byte offset).  Issued as inline assembly on purpose: the compiler tracks the builtin
+// form as an LDS write and then waits for it (vmcnt(0)) before every later LDS read it
+// cannot prove disjoint -- which would make the prefetched stages synchronous.  The kernel
+// orders these loads itself (see the pipeline below).  The "memory" clobber keeps the
+// compiler from moving LDS accesses across the issue.
+// A wave-uniform value in scalar registers (the asm operands below must be scalar even where
+// the compiler cannot prove uniformity itself).
+__device__ __forceinline__ const unsigned char* uniform_ptr(const void* p) {
+    const uint64_t v = reinterpret_cast<uintptr_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+    return reinterpret_cast<const unsigned char*>((static_cast<uint64_t>(hi) << 32) | lo);
 }
 
-// Where a tile's loads come from: wave-uniform scalars, set once per tile.
-struct TileSrc {
-    const bf16_t* a;   // activation rows (x_perm or H)
-    const bf16_t* b0;  // this expert's weights (W1^T or W2^T)
-    const bf16_t* b1;  // SwiGLU: this expert's W3^T
-    int64_t row0, last;  // first row of the tile, last valid row to read
-    int n0;              // first weight row (output column) of the tile
-};
+__device__ __forceinline__ void load_lds16(const unsigned char* base, uint32_t voff, uint32_t lds_addr) {
+    base = uniform_ptr(base);
+    lds_addr = __builtin_amdgcn_readfirstlane(lds_addr);
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds_addr), "v"(voff), "s"(base)
+                 : "memory", "m0");
+}
 
-// One stage of a wave's loads: 1 KiB per load, lane l landing at byte 16 l of it.  Load j
-// of wave w fills LDS rows (4 j + w) * RPI ..., so whether a load carries activation rows
-// or weight rows (and which weight matrix) is fixed by j at compile time.  LDS row R of the
-// stage holds activation row R (R < BM) or weight row R - BM; rows past the segment or past
-// N are clamped to a valid row, whose results are never stored.  Addresses are computed
-// here from the tile scalars rather than cached, to keep registers for the accumulators.
-template <int BM, int BN, int LPW, int RPI, int CPR, int SH>
-__device__ __forceinline__ void issue_stage(const TileSrc& ts, int K, int N, int wave, int lane, bf16_t* stage,
-                                            int k0) {
-    const int r_lane = lane / CPR, c_lane = lane % CPR;
+// One accumulator value for the epilogue.  With 256 accumulator registers per lane they
+// live in AGPRs, and VALU work needs them in VGPRs; left to itself the compiler copies all of
+// them at once when the K loop ends, which needs every VGPR and spills the loop's live
+// values.  Reading them one at a time keeps the epilogue's VGPR use small.
+template <bool IN_AGPR>
+__device__ __forceinline__ float acc_read(float a) {
+    if (!IN_AGPR) return a;
+    float v;
+    asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(a));
+    return v;
+}
+
+// Ask the scheduler to spread a step's LDS fragment reads between its MFMAs (one read after
+// every M / R MFMAs) instead of issuing them as one burst: a burst holds up the next MFMA
+// issue, and with one or two waves per SIMD nothing else fills the matrix core meanwhile.
+template <int M, int R>
+__device__ __forceinline__ void interleave_reads() {
+    constexpr int per = M / R > 0 ? M / R : 1;
 #pragma unroll
-    for (int j = 0; j < LPW; ++j) {
-        constexpr int kRowsPerJ = 4 * RPI;
-        const int R = (j * 4 + wave) * RPI + r_lane;
-        const int kc = c_lane ^ ((R >> SH) & (CPR - 1));
-        const bf16_t* src;
-        if (j * kRowsPerJ < BM) {
-            src = ts.a + min(ts.row0 + R, ts.last) * K;
-        } else {
-            constexpr int kAJ = BM / kRowsPerJ;  // loads per wave that carry activation rows
-            const int nb = ((j - kAJ) * kRowsPerJ) / BN;  // compile-time after unrolling
-            const int n = min(ts.n0 + (R - BM - nb * BN), N - 1);
-            src = (nb ? ts.b1 : ts.b0) + static_cast<int64_t>(n) * K;
-        }
-        load_lds16(src + k0 + kc * 8, stage + (j * 4 + wave) * RPI * (CPR * 8));
+    for (int k = 0; k < R; ++k) {
+        __builtin_amdgcn_sched_group_barrier(0x008, per, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // LDS read
     }
+    __builtin_amdgcn_sched_group_barrier(0x008, M - per * R > 0 ? M - per * R : 0, 0);
 }
 
 // Bare workgroup barrier.  A fenced barrier (__syncthreads, or even an LDS-only fence)
 // makes the compiler wait for every direct-to-LDS load in flight, which would drain the
-// prefetched stages this pipeline keeps in flight across the barrier.  Ordering is kept
-// by hand instead: each wave waits (wait_stages) for its own loads of the stage it is about
-// to read before arriving, so after the barrier that stage is complete for all waves; and
-// a wave only overwrites a stage buffer after the barrier that follows every wave's reads
-// of it (its ds_reads have returned: their data fed the MFMAs before the wave arrived).
-__device__ __forceinline__ void stage_barrier() { __builtin_amdgcn_s_barrier(); }
+// prefetched stages this pipeline keeps in flight across the barrier.  The empty asm
+// statements with a memory clobber keep the compiler from moving LDS reads across it.
+__device__ __forceinline__ void stage_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
 
-// Row tile mt's expert and row range, and the column offset of column tile nt.
+// Row tile mt's expert and row range.
 struct TileRows {
     int64_t row0, row_end;
     int e;
@@ -413,9 +418,11 @@ struct TileRows {
 template <int BM>
 __device__ __forceinline__ TileRows tile_rows(const GroupedGemm& g, const int* tstart, int mt) {
     TileRows t;
-    t.e = find_expert(tstart, g.E, mt);
-    t.row0 = g.offsets[t.e] + static_cast<int64_t>(mt - tstart[t.e]) * BM;
-    t.row_end = g.offsets[t.e + 1] < g.rows_max ? g.offsets[t.e + 1] : g.rows_max;
+    t.e = __builtin_amdgcn_readfirstlane(find_expert(tstart, g.E, mt));
+    const int first = __builtin_amdgcn_readfirstlane(tstart[t.e]);
+    const int64_t seg0 = g.offsets[t.e], seg1 = g.offsets[t.e + 1];
+    t.row0 = seg0 + static_cast<int64_t>(mt - first) * BM;
+    t.row_end = seg1 < g.rows_max ? seg1 : g.rows_max;
     return t;
 }
 
@@ -430,21 +437,58 @@ __device__ __forceinline__ void tile_coords(int L, int total_m, int n_tiles, int
     mt = grp * GM + (rem - nt * gsz);
 }
 
+// Where a tile's rows are read from.  The tile reads BM activation rows starting at
+// row_base and BN weight rows starting at n_base, both shifted back from the tile's own
+// first row / column when the tile would run past the end of the buffer (so every load
+// stays inside it without a per-row check); the epilogue stores only the tile's own rows
+// [row0, row_end) and columns [n0, N).
+struct TileGeom {
+    int64_t row0, row_end, row_base;
+    int n0, n_base, e;
+};
+
+template <int BM, int BN>
+__device__ __forceinline__ TileGeom tile_geom(const GroupedGemm& g, const int* tstart, int total_m, int L) {
+    int mt, nt;
+    tile_coords(L, total_m, g.n_tiles, mt, nt);
+    const TileRows tr = tile_rows<BM>(g, tstart, mt);
+    TileGeom t;
+    t.e = tr.e;
+    t.row0 = tr.row0;
+    t.row_end = tr.row_end;
+    const int64_t top = g.rows_max > BM ? g.rows_max - BM : 0;
+    t.row_base = tr.row0 < 0 ? 0 : (tr.row0 > top ? top : tr.row0);
+    t.n0 = nt * BN;
+    const int ntop = g.N > BN ? g.N - BN : 0;
+    t.n_base = t.n0 > ntop ? ntop : t.n0;
+    return t;
+}
+
 // Persistent grouped GEMM.  The grid is a fixed number of workgroups (one or two per CU);
 // the tiles are dealt to the 8 XCDs in contiguous runs (the hardware deals workgroups
 // round-robin, so workgroup b sits on XCD b % 8) and, inside a run, round-robin to that
-// XCD's workgroups, so concurrently running tiles share rows or weights in its L2.  The
-// load pipeline runs across tile boundaries: while one tile's last K steps are multiplied
-// and its epilogue runs, the next tile's first stages are already in flight.
+// XCD's workgroups, so concurrently running tiles share rows or weights in its L2.
+//
+// Pipeline (per wave; stage b = the b-th K step this workgroup multiplies, counted across
+// tiles).  Loads run NS - 1 stages ahead, across tile boundaries.  Stage b is published by
+// one barrier: before it each wave waits for its own loads of stage b (vmcnt) and for its
+// own LDS reads of stage b - 1 (lgkmcnt); after it, stage b is complete for every wave and
+// nobody reads stage b - 1 any more, so its buffer is refilled with stage b + NS - 1 right
+// away.  Inside a tile, that barrier sits in front of the last MFMA step of stage b - 1:
+// the first fragments of stage b are read from LDS while those MFMAs run, and every other
+// MFMA step's fragments are read during the step before it (two fragment sets in
+// registers).  Every 1 KiB load has a fixed per-lane offset (computed once) from a scalar
+// base that moves by 2*BK bytes per stage.
 template <int BM, int BW, int BK, int NS, int EPI, bool OB>
-__global__ __launch_bounds__(kThreads, (LdsShape<BM, BW, BK, NS, EPI>::kBytes <= 80 * 1024) ? 2 : 1)
+__global__ __launch_bounds__(kThreads, (LdsShape<BM, BW, BK, NS, EPI>::kPerCU))
 void gemm_bf16_lds(GroupedGemm g) {
     typedef LdsShape<BM, BW, BK, NS, EPI> S;
     constexpr int NB = S::kNB, BN = S::kBN, MI = S::kMI, NI = S::kNI, ROWS = S::kRows, LPW = S::kLPW;
-    constexpr int CPR = S::kCPR, RPI = S::kRPI, SH = S::kSwzShift;
+    constexpr int CPR = S::kCPR, RPI = S::kRPI, SH = S::kSwzShift, KS = S::kKS;
+    constexpr int kStageBytes = ROWS * BK * 2;
+    constexpr int kAJ = BM / (4 * RPI);  // loads per wave per stage that carry activation rows
     __shared__ int tstart[kThreads + 1];
     extern __shared__ __align__(1024) unsigned char smem_raw[];
-    bf16_t* smem = reinterpret_cast<bf16_t*>(smem_raw);
 
     const int total_m = tile_prefix<BM>(g.offsets, g.E, tstart);
     const int total = total_m * g.n_tiles;
@@ -458,43 +502,85 @@ void gemm_bf16_lds(GroupedGemm g) {
     const int tid = threadIdx.x, lane = tid & 63;
     // the wave index is uniform across a wave; say so, so that per-wave choices stay scalar
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const bf16_t* __restrict__ A = static_cast<const bf16_t*>(g.a);
+    const uint32_t lds0 = __builtin_amdgcn_readfirstlane(
+        static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) void*)smem_raw)));
 
-    // ---- load cursor: tile lt, K step lk
-    int lt = t_first, lk = 0;
-    TileSrc ts;
-    auto set_tile = [&](int L) {
-        int mt, nt;
-        tile_coords(L, total_m, g.n_tiles, mt, nt);
-        const TileRows tr = tile_rows<BM>(g, tstart, mt);
-        ts.a = A;
-        ts.b0 = static_cast<const bf16_t*>(g.b) + tr.e * g.b_estride;
-        ts.b1 = NB > 1 ? static_cast<const bf16_t*>(g.b2) + tr.e * g.b_estride : ts.b0;
-        ts.row0 = max<int64_t>(0, tr.row0);
-        // rows past the segment are clamped to its last row; inconsistent offsets (a segment
-        // outside [0, rows_max)) still only ever read rows inside the buffer
-        int64_t last = tr.row_end > tr.row0 ? tr.row_end - 1 : tr.row0;
-        ts.last = max<int64_t>(0, min<int64_t>(last, g.rows_max - 1));
-        ts.n0 = nt * BN;
-    };
-    set_tile(lt);
-    int issued = 0;  // stages issued by this wave so far
+    // Per-lane byte offsets of this wave's loads: load j fills LDS rows (4 j + wave) * RPI
+    // + lane / CPR of a stage, slot lane % CPR, with global chunk slot ^ swz(row).  Rows past
+    // a buffer smaller than one tile repeat its last row.
+    uint32_t voff[LPW];
+    {
+        const int r_lane = lane / CPR, c_lane = lane % CPR;
+        const int a_lim = static_cast<int>(g.rows_max < BM ? g.rows_max : BM) - 1;
+        const int b_lim = (g.N < BN ? g.N : BN) - 1;
 #pragma unroll
-    for (int st = 0; st < NS - 1; ++st) {
-        if (lt < t_end) {
-            issue_stage<BM, BN, LPW, RPI, CPR, SH>(ts, g.K, g.N, wave, lane, smem + (issued % NS) * ROWS * BK, lk * BK);
-            ++issued;
-            if (++lk == nk) {
-                lk = 0;
-                lt += nslot;
-                if (lt < t_end) set_tile(lt);
-            }
+        for (int j = 0; j < LPW; ++j) {
+            const int R = (j * 4 + wave) * RPI + r_lane;
+            const int kc = c_lane ^ ((R >> SH) & (CPR - 1));
+            int r;
+            if (j < kAJ) r = min(R, a_lim);
+            else r = min((R - BM) % BN, b_lim);
+            voff[j] = static_cast<uint32_t>(r) * static_cast<uint32_t>(2 * g.K) + static_cast<uint32_t>(kc * 16);
         }
     }
 
-    // ---- compute: one tile after another; the load cursor above runs NS - 1 stages ahead
+    // ---- load cursor: tile lt, K step lk, scalar bases of the tile's rows at K = 0
+    int lt = t_first, lk = 0;
+    const unsigned char *src_a = nullptr, *src_b0 = nullptr, *src_b1 = nullptr;
+    auto set_tile = [&](int L) {
+        const TileGeom t = tile_geom<BM, BN>(g, tstart, total_m, L);
+        const int64_t rb = 2 * static_cast<int64_t>(g.K);
+        src_a = uniform_ptr(static_cast<const unsigned char*>(g.a) + t.row_base * rb);
+        const int64_t boff = (t.e * g.b_estride) * 2 + t.n_base * rb;
+        src_b0 = uniform_ptr(static_cast<const unsigned char*>(g.b) + boff);
+        src_b1 = NB > 1 ? uniform_ptr(static_cast<const unsigned char*>(g.b2) + boff) : src_b0;
+    };
+    int issued = 0;  // stages issued by this wave so far
+    auto issue_next = [&]() {
+        if (lt >= t_end) return;
+        const uint32_t dst = lds0 + (issued % NS) * kStageBytes;
+        const int kb = lk * BK * 2;
+#pragma unroll
+        for (int j = 0; j < LPW; ++j) {
+            const unsigned char* base = j < kAJ ? src_a : ((NB > 1 && (j - kAJ) * 4 * RPI >= BN) ? src_b1 : src_b0);
+            load_lds16(base + kb, voff[j], dst + (j * 4 + wave) * RPI * CPR * 16);
+        }
+        ++issued;
+        if (++lk == nk) {
+            lk = 0;
+            lt += nslot;
+            if (lt < t_end) set_tile(lt);
+        }
+    };
+    set_tile(lt);
+#pragma unroll
+    for (int st = 0; st < NS - 1; ++st) issue_next();
+
+    // ---- fragments: A block i = activation rows wm*BM/2 + 32 i + l32, B block (nb, j) =
+    // weight rows BM + nb*BN + wn*BN/2 + 32 j + l32; K chunk 2 ks + lhi of the stage
     const int wm = wave >> 1, wn = wave & 1;
     const int l32 = lane & 31, lhi = lane >> 5;
+    typedef bf16x8_t Frags[MI + NB * NI];
+    auto read_frags = [&](int stage_slot, int ks, Frags& f) {
+        const unsigned char* st = smem_raw + stage_slot * kStageBytes;
+        const int ch = 2 * ks + lhi;
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+            const int R = wm * (BM / 2) + i * 32 + l32;
+            f[i] = *reinterpret_cast<const bf16x8_t*>(st + R * (2 * BK) + ((ch ^ ((R >> SH) & (CPR - 1))) << 4));
+        }
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int j = 0; j < NI; ++j) {
+                const int R = BM + nb * BN + wn * (BN / 2) + j * 32 + l32;
+                f[MI + nb * NI + j] =
+                    *reinterpret_cast<const bf16x8_t*>(st + R * (2 * BK) + ((ch ^ ((R >> SH) & (CPR - 1))) << 4));
+            }
+    };
+
+    // one workgroup per CU: the accumulators fill the AGPRs (see acc_read)
+    constexpr bool kAccInAgpr = S::kPerCU == 1;
     int consumed = 0;
     for (int ct = t_first; ct < t_end; ct += nslot) {
         f32x16_t acc[NB][MI][NI];
@@ -506,71 +592,68 @@ void gemm_bf16_lds(GroupedGemm g) {
                 for (int j = 0; j < NI; ++j)
 #pragma unroll
                     for (int r = 0; r < 16; ++r) acc[nb][i][j][r] = 0.f;
+        auto mma = [&](const Frags& f) {
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+#pragma unroll
+                    for (int j = 0; j < NI; ++j)
+                        acc[nb][i][j] =
+                            __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[MI + nb * NI + j], f[i], acc[nb][i][j], 0, 0, 0);
+        };
+
+        // publish the tile's first stage; after an epilogue its stores share the counter
+        if (ct != t_first) wait_vmcnt<0>();
+        else wait_stages<LPW, NS>(issued - consumed - 1);
+        stage_barrier();
+        issue_next();
+        Frags f0, f1;
+        read_frags(consumed % NS, 0, f0);
 
         for (int ck = 0; ck < nk; ++ck) {
-            // the first step after an epilogue also waits for its stores (they share the counter)
-            if (ck == 0 && ct != t_first) wait_vmcnt<0>();
-            else wait_stages<LPW, NS>(issued - consumed - 1);
-            stage_barrier();
-            if (lt < t_end) {
-                issue_stage<BM, BN, LPW, RPI, CPR, SH>(ts, g.K, g.N, wave, lane, smem + (issued % NS) * ROWS * BK,
-                                                       lk * BK);
-                ++issued;
-                if (++lk == nk) {
-                    lk = 0;
-                    lt += nslot;
-                    if (lt < t_end) set_tile(lt);
+            const int slot = consumed % NS;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                Frags& cur = (ks & 1) ? f1 : f0;
+                Frags& nxt = (ks & 1) ? f0 : f1;
+                if (ks + 1 < KS) {
+                    read_frags(slot, ks + 1, nxt);
+                } else if (ck + 1 < nk) {
+                    // publish stage consumed + 1 (see above), refill, start its fragments
+                    wait_lgkm0();
+                    wait_stages<LPW, NS>(issued - consumed - 2);
+                    stage_barrier();
+                    issue_next();
+                    read_frags((consumed + 1) % NS, 0, nxt);
                 }
+                mma(cur);
+                interleave_reads<NB * MI * NI, MI + NB * NI>();
             }
-            const bf16_t* st = smem + (consumed % NS) * ROWS * BK;
-#pragma unroll
-            for (int ks = 0; ks < BK / 16; ++ks) {
-                const int ch = 2 * ks + lhi;
-                bf16x8_t af[MI], wf[NB][NI];
-#pragma unroll
-                for (int i = 0; i < MI; ++i) {
-                    const int R = wm * (BM / 2) + i * 32 + l32;
-                    af[i] = *reinterpret_cast<const bf16x8_t*>(st + R * BK + ((ch ^ ((R >> SH) & (CPR - 1))) << 3));
-                }
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                    for (int j = 0; j < NI; ++j) {
-                        const int R = BM + nb * BN + wn * (BN / 2) + j * 32 + l32;
-                        wf[nb][j] = *reinterpret_cast<const bf16x8_t*>(st + R * BK + ((ch ^ ((R >> SH) & (CPR - 1))) << 3));
-                    }
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                    for (int i = 0; i < MI; ++i)
-#pragma unroll
-                        for (int j = 0; j < NI; ++j)
-                            acc[nb][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[nb][j], af[i], acc[nb][i][j], 0, 0, 0);
-            }
+            // KS is even for BK 32 / 64, so the next step's first fragments are in f0
             ++consumed;
         }
 
         // ---- epilogue of tile ct.  D[n][m] layout: lane holds activation row l32 of the
         // block; register r holds weight row 8 * (r / 4) + 4 * lhi + r % 4, i.e. 4
         // consecutive output columns per group r / 4.
-        int mt, nt;
-        tile_coords(ct, total_m, g.n_tiles, mt, nt);
-        const TileRows tr = tile_rows<BM>(g, tstart, mt);
-        const int n0 = nt * BN;
+        const TileGeom t = tile_geom<BM, BN>(g, tstart, total_m, ct);
+        const int64_t row_lo = t.row0 > 0 ? t.row0 : 0;
 #pragma unroll
         for (int i = 0; i < MI; ++i) {
-            const int64_t row = tr.row0 + wm * (BM / 2) + i * 32 + l32;
-            const bool row_ok = row >= 0 && row < tr.row_end;
+            const int64_t row = t.row_base + wm * (BM / 2) + i * 32 + l32;
+            const bool row_ok = row >= row_lo && row < t.row_end;
 #pragma unroll
             for (int j = 0; j < NI; ++j)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int col = n0 + wn * (BN / 2) + j * 32 + 8 * q + 4 * lhi;
+                    const int col = t.n_base + wn * (BN / 2) + j * 32 + 8 * q + 4 * lhi;
                     float v[4];
 #pragma unroll
                     for (int c = 0; c < 4; ++c)
-                        v[c] = epilogue_fast<EPI>(acc[0][i][j][4 * q + c], acc[NB - 1][i][j][4 * q + c]);
-                    if (row_ok && col < g.N) {
+                        v[c] = epilogue_fast<EPI>(acc_read<kAccInAgpr>(acc[0][i][j][4 * q + c]),
+                                                  acc_read<kAccInAgpr>(acc[NB - 1][i][j][4 * q + c]));
+                    if (row_ok && col >= t.n0 && col < g.N) {
                         if (OB) {
                             uint2 pk;
                             pk.x = pack_bf16x2(v[0], v[1]);
@@ -588,7 +671,6 @@ void gemm_bf16_lds(GroupedGemm g) {
         }
     }
 }
-
 // ------------------------------------------------------------------ fp32 kernel
 
 constexpr int kFBM = 64, kFBN = 64, kFBK = 16;
@@ -723,7 +805,7 @@ template <int BM, int BW, int BK, int NS, int EPI, bool OB>
 hipError_t run_bf16_lds(GroupedGemm g, int64_t A_max, hipStream_t s) {
     typedef LdsShape<BM, BW, BK, NS, EPI> S;
     constexpr size_t lds = S::kBytes;
-    constexpr int per_cu = (lds <= 80 * 1024) ? 2 : 1;
+    constexpr int per_cu = S::kPerCU;
     static const hipError_t attr = hipFuncSetAttribute(
         reinterpret_cast<const void*>(&gemm_bf16_lds<BM, BW, BK, NS, EPI, OB>),
         hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
@@ -743,7 +825,9 @@ hipError_t run_bf16_lds(GroupedGemm g, int64_t A_max, hipStream_t s) {
 // pipeline fill overlap the other's MFMAs.
 template <int EPI, bool OB>
 hipError_t run_bf16_best(GroupedGemm g, int64_t A_max, hipStream_t s) {
-    if (g.K % 32 == 0) return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);
+    // per-lane load offsets are 32-bit: 256 rows of K elements must span less than 4 GiB
+    if (g.K % 32 == 0 && static_cast<int64_t>(g.K) * 2 * 256 < (int64_t(1) << 32))
+        return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);
     return run_bf16<EPI, OB>(g, A_max, s);
 }
 
