@@ -118,13 +118,16 @@ size_t moe_packed_weights_size(int32_t E, int64_t h, int64_t f, moe_act act, moe
  *   packed  moe_packed_weights_size(...) bytes.  Layout (internal, may change):
  *           W1^T [E][fp][h], (W3^T [E][fp][h]), W2^T [E][h][fp], fp = padded f;
  *           padded inner columns are zero, which is exact: every activation maps 0 to 0.
+ *           bf16 matrices are stored K-blocked (K = the second index: element (r, k) of
+ *           an [R][K] matrix at ((k / 32) * R + r) * 32 + k % 32), W1^T / W3^T only when
+ *           h % 32 == 0; fp32 matrices are row-major.
  * Run once per shard; the result is read-only for moe_expert_ffn_shard. */
 moe_status moe_pack_weights(const void *w1, const void *w3, const void *w2, int32_t E,
                             int64_t h, int64_t F, int64_t col0, int64_t f, moe_act act,
                             moe_dtype wdt, void *packed, size_t packed_bytes,
                             hipStream_t stream);
 
-/* Bytes of workspace moe_expert_ffn_shard needs (the activated inner rows). */
+/* Bytes of workspace moe_expert_ffn_shard needs (the activated inner rows, A_max x fp). */
 size_t moe_ffn_workspace_size(int64_t A_max, int32_t E, int64_t h, int64_t f, moe_act act,
                               moe_dtype dt);
 

@@ -129,7 +129,9 @@ constexpr size_t bf_lds_bytes() {
                : bf_cstage_bytes<OB>(BfShape<EPI>::kBN);
 }
 
-template <int EPI, bool OB>
+// CB: C is stored K-blocked for the next GEMM (element (row, n) at
+// ((n / 32) * rows_max + row) * 32 + n % 32), else row-major with stride ldc.
+template <int EPI, bool OB, bool CB>
 __global__ __launch_bounds__(kThreads, 2) void gemm_bf16(GroupedGemm g) {
     typedef BfShape<EPI> S;
     constexpr int NB = S::kNB, JN = S::kJN, BN = S::kBN;
@@ -265,9 +267,10 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16(GroupedGemm g) {
         for (int q = 0; q < kBM * VPR / kThreads; ++q) {
             const int v = tid + q * kThreads;
             const int row = v / VPR, c8 = (v % VPR) * 8;
-            if (row0 + row < row_end && n0 + c8 < g.N)
-                *reinterpret_cast<uint4*>(C + (row0 + row) * g.ldc + n0 + c8) =
-                    *reinterpret_cast<const uint4*>(cs + row * LDC + c8);
+            const int64_t n = n0 + c8;
+            const int64_t ci = CB ? ((n >> 5) * g.rows_max + row0 + row) * 32 + (n & 31) : (row0 + row) * g.ldc + n;
+            if (row0 + row < row_end && n < g.N)
+                *reinterpret_cast<uint4*>(C + ci) = *reinterpret_cast<const uint4*>(cs + row * LDC + c8);
         }
     } else {
         constexpr int LDC = BN + 4;
@@ -289,9 +292,10 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16(GroupedGemm g) {
         for (int q = 0; q < kBM * VPR / kThreads; ++q) {
             const int v = tid + q * kThreads;
             const int row = v / VPR, c4 = (v % VPR) * 4;
-            if (row0 + row < row_end && n0 + c4 < g.N)
-                *reinterpret_cast<float4*>(C + (row0 + row) * g.ldc + n0 + c4) =
-                    *reinterpret_cast<const float4*>(cs + row * LDC + c4);
+            const int64_t n = n0 + c4;
+            const int64_t ci = CB ? ((n >> 5) * g.rows_max + row0 + row) * 32 + (n & 31) : (row0 + row) * g.ldc + n;
+            if (row0 + row < row_end && n < g.N)
+                *reinterpret_cast<float4*>(C + ci) = *reinterpret_cast<const float4*>(cs + row * LDC + c4);
         }
     }
 }
@@ -299,14 +303,17 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16(GroupedGemm g) {
 // ------------------------------------------------------------------ bf16 MFMA kernel, direct-to-LDS pipeline
 //
 // Tile: BM activation rows x BW weight rows (SwiGLU: BW/2 rows of W1 + the same rows of
-// W3), K in steps of BK (32 or 64).  A row's BK-element slice is one LDS row of 2*BK bytes
-// holding CPR = BK/8 chunks of 16 bytes; chunk c of row r is stored at position
-// c ^ swz(r), which keeps the 32-row MFMA fragment reads free of bank conflicts.  Global
-// data goes straight to LDS with global_load_lds_dwordx4 (lane l of a wave instruction
-// fills bytes [16 l, 16 l + 16) of a 1 KiB span), NS stages deep.  The weight fragment is
+// W3), K in steps of BK = 32.  A row's 32-element slice is one LDS row of 64 bytes holding
+// 4 chunks of 16 bytes; chunk c of row r is stored at position c ^ swz(r), which keeps the
+// 32-row MFMA fragment reads free of bank conflicts.  Global data goes straight to LDS with
+// global_load_lds_dwordx4 (lane l of a wave instruction fills bytes [16 l, 16 l + 16) of a
+// 1 KiB span: 16 LDS rows), NS stages deep.  The weights are K-blocked (see the pack step:
+// a stage's rows are one contiguous run), and so is the intermediate H, which the
+// up-projection writes and the down-projection reads: every 1 KiB load of those operands
+// is 1 KiB of contiguous memory, eight full 128-byte lines.  The up-projection's
+// activations (x_perm) are row-major: 64-byte pieces of 16 rows.  The weight fragment is
 // the MFMA's first operand, so each lane ends up holding 4 consecutive output columns of
-// one row (one 8- or 16-byte store per group).  K must be a multiple of BK and N (per
-// weight matrix) a multiple of the tile's columns, or at most one tile wide.
+// one row (one 8- or 16-byte store per group).  K must be a multiple of 32.
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -346,7 +353,7 @@ struct LdsShape {
     static_assert(kMI >= 1 && kNI >= 1, "tile too small for 2 x 2 waves of 32 x 32 blocks");
     static_assert(kRows % (kRPI * 4) == 0, "stage rows must split evenly over the waves");
     static_assert(BM % (4 * kRPI) == 0 && kBN % (4 * kRPI) == 0, "a wave load carries one kind of row");
-    static_assert(BK == 32 || BK == 64, "BK");
+    static_assert(BK == 32, "the K-blocked operands come in blocks of 32");
 };
 
 // 16 bytes per lane from global memory straight into LDS: lane l's bytes come from
@@ -479,10 +486,14 @@ __device__ __forceinline__ TileGeom tile_geom(const GroupedGemm& g, const int* t
 // MFMA step's fragments are read during the step before it (two fragment sets in
 // registers).  Every 1 KiB load has a fixed per-lane offset (computed once) from a scalar
 // base that moves by 2*BK bytes per stage.
+//
+// The activation epilogues belong to the up-projection (A = x_perm row-major, C = H
+// K-blocked); the plain one to the down-projection (A = H K-blocked, C = y_perm row-major).
 template <int BM, int BW, int BK, int NS, int EPI, bool OB>
 __global__ __launch_bounds__(kThreads, (LdsShape<BM, BW, BK, NS, EPI>::kPerCU))
 void gemm_bf16_lds(GroupedGemm g) {
     typedef LdsShape<BM, BW, BK, NS, EPI> S;
+    constexpr bool kUp = EPI != kEpiNone;
     constexpr int NB = S::kNB, BN = S::kBN, MI = S::kMI, NI = S::kNI, ROWS = S::kRows, LPW = S::kLPW;
     constexpr int CPR = S::kCPR, RPI = S::kRPI, SH = S::kSwzShift, KS = S::kKS;
     constexpr int kStageBytes = ROWS * BK * 2;
@@ -520,7 +531,8 @@ void gemm_bf16_lds(GroupedGemm g) {
             int r;
             if (j < kAJ) r = min(R, a_lim);
             else r = min((R - BM) % BN, b_lim);
-            voff[j] = static_cast<uint32_t>(r) * static_cast<uint32_t>(2 * g.K) + static_cast<uint32_t>(kc * 16);
+            const uint32_t row_bytes = (j < kAJ && kUp) ? static_cast<uint32_t>(2 * g.K) : 64u;
+            voff[j] = static_cast<uint32_t>(r) * row_bytes + static_cast<uint32_t>(kc * 16);
         }
     }
 
@@ -529,9 +541,9 @@ void gemm_bf16_lds(GroupedGemm g) {
     const unsigned char *src_a = nullptr, *src_b0 = nullptr, *src_b1 = nullptr;
     auto set_tile = [&](int L) {
         const TileGeom t = tile_geom<BM, BN>(g, tstart, total_m, L);
-        const int64_t rb = 2 * static_cast<int64_t>(g.K);
+        const int64_t rb = kUp ? 2 * static_cast<int64_t>(g.K) : 64;
         src_a = uniform_ptr(static_cast<const unsigned char*>(g.a) + t.row_base * rb);
-        const int64_t boff = (t.e * g.b_estride) * 2 + t.n_base * rb;
+        const int64_t boff = (t.e * g.b_estride) * 2 + static_cast<int64_t>(t.n_base) * 64;
         src_b0 = uniform_ptr(static_cast<const unsigned char*>(g.b) + boff);
         src_b1 = NB > 1 ? uniform_ptr(static_cast<const unsigned char*>(g.b2) + boff) : src_b0;
     };
@@ -539,11 +551,14 @@ void gemm_bf16_lds(GroupedGemm g) {
     auto issue_next = [&]() {
         if (lt >= t_end) return;
         const uint32_t dst = lds0 + (issued % NS) * kStageBytes;
-        const int kb = lk * BK * 2;
+        // K block lk of each operand: the next 64 bytes of every row (row-major x_perm), or
+        // the next block of all rows (K-blocked)
+        const int64_t ka = kUp ? static_cast<int64_t>(lk) * 64 : static_cast<int64_t>(lk) * g.rows_max * 64;
+        const int64_t kb = static_cast<int64_t>(lk) * g.N * 64;
 #pragma unroll
         for (int j = 0; j < LPW; ++j) {
-            const unsigned char* base = j < kAJ ? src_a : ((NB > 1 && (j - kAJ) * 4 * RPI >= BN) ? src_b1 : src_b0);
-            load_lds16(base + kb, voff[j], dst + (j * 4 + wave) * RPI * CPR * 16);
+            const unsigned char* base = j < kAJ ? src_a + ka : ((NB > 1 && (j - kAJ) * 4 * RPI >= BN) ? src_b1 : src_b0) + kb;
+            load_lds16(base, voff[j], dst + (j * 4 + wave) * RPI * CPR * 16);
         }
         ++issued;
         if (++lk == nk) {
@@ -654,14 +669,16 @@ void gemm_bf16_lds(GroupedGemm g) {
                         v[c] = epilogue_fast<EPI>(acc_read<kAccInAgpr>(acc[0][i][j][4 * q + c]),
                                                   acc_read<kAccInAgpr>(acc[NB - 1][i][j][4 * q + c]));
                     if (row_ok && col >= t.n0 && col < g.N) {
+                        // 4 columns col .. col + 3 never cross a 32-column block
+                        const int64_t ci = kUp ? ((static_cast<int64_t>(col) >> 5) * g.rows_max + row) * 32 + (col & 31)
+                                               : row * g.ldc + col;
                         if (OB) {
                             uint2 pk;
                             pk.x = pack_bf16x2(v[0], v[1]);
                             pk.y = pack_bf16x2(v[2], v[3]);
-                            *reinterpret_cast<uint2*>(static_cast<bf16_t*>(g.c) + row * g.ldc + col) = pk;
+                            *reinterpret_cast<uint2*>(static_cast<bf16_t*>(g.c) + ci) = pk;
                         } else {
-                            *reinterpret_cast<float4*>(static_cast<float*>(g.c) + row * g.ldc + col) =
-                                make_float4(v[0], v[1], v[2], v[3]);
+                            *reinterpret_cast<float4*>(static_cast<float*>(g.c) + ci) = make_float4(v[0], v[1], v[2], v[3]);
                         }
                     }
                     // one block at a time: keeps the scheduler from pulling every accumulator
@@ -763,21 +780,21 @@ int64_t row_tile_bound(int64_t A_max, int E, int bm) {
     return b < A_max ? b : A_max;
 }
 
-template <int EPI, bool OB>
+template <int EPI, bool OB, bool CB>
 hipError_t run_bf16(GroupedGemm g, int64_t A_max, hipStream_t s) {
     typedef BfShape<EPI> S;
     constexpr size_t lds = bf_lds_bytes<EPI, OB>();
     static std::once_flag once;
     static hipError_t attr_err = hipSuccess;
     std::call_once(once, [] {
-        attr_err = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16<EPI, OB>),
+        attr_err = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16<EPI, OB, CB>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
     });
     if (attr_err != hipSuccess) return attr_err;
     g.n_tiles = static_cast<int>(ceil_div(g.N, S::kBN));
     const int64_t blocks = row_tile_bound(A_max, g.E, kBM) * g.n_tiles;
     if (blocks == 0) return hipSuccess;
-    hipLaunchKernelGGL((gemm_bf16<EPI, OB>), dim3(static_cast<unsigned>(blocks)), dim3(kThreads), lds, s, g);
+    hipLaunchKernelGGL((gemm_bf16<EPI, OB, CB>), dim3(static_cast<unsigned>(blocks)), dim3(kThreads), lds, s, g);
     return hipGetLastError();
 }
 
@@ -823,12 +840,16 @@ hipError_t run_bf16_lds(GroupedGemm g, int64_t A_max, hipStream_t s) {
 // Tile shape: 128 activation rows x 256 weight rows, 32-wide K steps, three stages (two in
 // flight) in 72 KiB of LDS, so that two workgroups share a CU and one's epilogue and
 // pipeline fill overlap the other's MFMAs.
+//
+// The up-projection needs h % 32 == 0 for the pipelined kernel (the packed W1 is K-blocked
+// exactly then); otherwise the register-staged kernel runs it on row-major weights and still
+// writes H K-blocked.  The down-projection's K is fp, always a multiple of 128.
 template <int EPI, bool OB>
 hipError_t run_bf16_best(GroupedGemm g, int64_t A_max, hipStream_t s) {
-    // per-lane load offsets are 32-bit: 256 rows of K elements must span less than 4 GiB
-    if (g.K % 32 == 0 && static_cast<int64_t>(g.K) * 2 * 256 < (int64_t(1) << 32))
-        return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);
-    return run_bf16<EPI, OB>(g, A_max, s);
+    constexpr bool kUp = EPI != kEpiNone;
+    if (g.K % 32 == 0) return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);
+    if (kUp) return run_bf16<EPI, OB, true>(g, A_max, s);
+    return hipErrorInvalidValue;  // not reachable through the C ABI (fp % 128 == 0)
 }
 
 template <int EPI>
