@@ -847,8 +847,11 @@ hipError_t run_bf16_lds(GroupedGemm g, int64_t A_max, hipStream_t s) {
 template <int EPI, bool OB>
 hipError_t run_bf16_best(GroupedGemm g, int64_t A_max, hipStream_t s) {
     constexpr bool kUp = EPI != kEpiNone;
-    if (g.K % 32 == 0) return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);
-    if (kUp) return run_bf16<EPI, OB, true>(g, A_max, s);
+    if (kUp) {
+        if (g.K % 32 == 0) return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);
+        return run_bf16<EPI, OB, true>(g, A_max, s);
+    }
+    if (g.K % 32 == 0) return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);  // down-projection
     return hipErrorInvalidValue;  // not reachable through the C ABI (fp % 128 == 0)
 }
 
