@@ -4,6 +4,7 @@ One step = one full layer forward (route -> dispatch -> expert FFN shard -> comb
 one batch of synthetic tokens already resident in HBM.  Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--config c2] [--no-cpu-baseline]
+  python bench.py --ablation        # grouped vs per-expert launches, E = 8 .. 256
 
 HBM traffic of the expert-FFN kernels comes from two rocprofv3 counter runs of this script,
 one with --pmc FETCH_SIZE and one with --pmc WRITE_SIZE, each with --copy-probe-mib so that
@@ -102,6 +103,58 @@ def summarize_counters(config: str, fetch_dir: str, write_dir: str, probe_mib: i
     print(json.dumps(rec, indent=1))
 
 
+def ablation_per_expert(seed: int, reps: int, experts):
+    """The grouped single launch against one launch pair per expert (the expert step with
+    and without the grouped formulation), on the paper's evaluation shape: b = 250, s = 120
+    (30 000 tokens), h = 768, one device's 1/4 shard of a 3072-wide FFN, top-1, skewed
+    router with k_r = ceil(0.1 E) hot experts and alpha_r = 0.6.  One JSON line per E."""
+    import math
+    import torch
+    import paper_2503_08467_amd as moe
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    base = synth.CONFIGS["paper128"]
+    for E in experts:
+        cfg = base.with_(name=f"paper{E}", E=E, routing=("paper", math.ceil(0.1 * E), 0.6))
+        L = synth.make(cfg, seed=seed)
+        to = lambda a, d=torch.bfloat16: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(d)
+        x, wg, bias = to(L.x), to(L.wg), to(L.sel_bias, torch.float32)
+        packed = moe.pack_weights(to(L.w1), to(L.w2), act=cfg.act)
+        del L
+        idx, w = moe.route(x, wg, cfg.k, bias, False)
+        disp = moe.dispatch(idx, x, E)
+        out = torch.empty_like(disp.x_perm)
+        ws = torch.empty(moe.ffn_workspace_size(cfg.A, packed), dtype=torch.uint8, device=dev)
+        touched = int((disp.counts > 0).sum().item())
+
+        def timed(fn):
+            for _ in range(3):
+                fn()
+            torch.cuda.synchronize()
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            t0 = time.perf_counter()
+            ev[0].record(stream)
+            for _ in range(reps):
+                fn()
+            ev[1].record(stream)
+            torch.cuda.synchronize()
+            return ev[0].elapsed_time(ev[1]) * 1e3 / reps, (time.perf_counter() - t0) * 1e6 / reps
+
+        g_us, g_wall = timed(lambda: moe.expert_ffn_shard(disp.x_perm, disp.offsets, packed, out=out, ws=ws))
+        # the per-expert loop reads the counts back on every call, as it must to size its launches
+        p_us, p_wall = timed(lambda: moe.expert_ffn_shard_per_expert(disp.x_perm, disp.offsets, packed, out=out,
+                                                                     ws=ws))
+        print(json.dumps({"ablation": "grouped vs per-expert launches", "experts": E, "tokens": cfg.T,
+                          "hidden": cfg.h, "shard_inner_width": cfg.f, "hot_experts": math.ceil(0.1 * E),
+                          "touched_experts": touched, "grouped_ffn_us": round(g_us, 1),
+                          "per_expert_ffn_us": round(p_us, 1), "per_expert_wall_us": round(p_wall, 1),
+                          "speedup": round(p_us / g_us, 2), "launches_grouped": 2,
+                          "launches_per_expert": 2 * touched}), flush=True)
+        del packed, x, wg, bias, idx, w, disp, out, ws
+        torch.cuda.empty_cache()
+
+
 def cpu_baseline(cfg_name: str, seed: int, budget_s: float = 12.0):
     """The fp64 oracle on a bounded sample of the same workload (its first tokens)."""
     import oracle
@@ -143,9 +196,14 @@ def main():
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run an untimed plain copy of this size first (counter calibration)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--ablation", action="store_true",
+                    help="grouped launch vs one launch pair per expert over E = 8 .. 256 (paper's shape)")
     args = ap.parse_args()
     if args.summarize_counters:
         summarize_counters(args.config, *args.summarize_counters, probe_mib=args.copy_probe_mib or 256)
+        return
+    if args.ablation:
+        ablation_per_expert(args.seed, reps=max(args.steps // 5, 5), experts=(8, 16, 32, 64, 128, 256))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this layer's multi-GPU exchange is not built, so only "

@@ -148,6 +148,21 @@ moe_status moe_expert_ffn_shard(const void *x_perm, const int32_t *offsets, int6
                                 const void *packed, void *y_perm, moe_dtype ydt, void *ws,
                                 size_t ws_bytes, hipStream_t stream);
 
+/* Ablation of the single grouped operation (Section 3.3's second optimization, the one the
+ * paper's ablation study removes): the same result as moe_expert_ffn_shard, bit for bit,
+ * computed with one launch of each matmul per expert that has rows -- Step 4's per-expert
+ * loop without the grouped formulation.  The launches are sized from a host copy of the
+ * offsets, so the caller reads them back first (the synchronization such a loop needs).
+ * Arguments as moe_expert_ffn_shard, plus
+ *   offsets_host [E+1] int32 in host memory, equal to the device offsets: nondecreasing,
+ *                offsets_host[0] >= 0 and offsets_host[E] <= A_max, else
+ *                MOE_ERR_INVALID_ARG (nothing is launched). */
+moe_status moe_expert_ffn_shard_per_expert(const void *x_perm, const int32_t *offsets,
+                                           const int32_t *offsets_host, int64_t A_max, int32_t E,
+                                           int64_t h, int64_t f, moe_act act, moe_dtype dt,
+                                           const void *packed, void *y_perm, moe_dtype ydt,
+                                           void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* Step 5 (Algorithm 1, aggregateTokens): point-wise weighted sum of each token's expert
  * results, accumulated in fp32 in pick order j = 0..k-1 and rounded once:
  *     y[t] = sum_j topk_w[t, j] * y_perm[pos_of[t, j]]

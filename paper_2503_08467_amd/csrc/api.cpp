@@ -129,9 +129,9 @@ size_t moe_ffn_workspace_size(int64_t A_max, int32_t E, int64_t h, int64_t f, mo
            kAlign;
 }
 
-moe_status moe_expert_ffn_shard(const void* x_perm, const int32_t* offsets, int64_t A_max, int32_t E, int64_t h,
-                                int64_t f, moe_act act, moe_dtype dt, const void* packed, void* y_perm,
-                                moe_dtype ydt, void* ws, size_t ws_bytes, hipStream_t stream) {
+static moe_status ffn_check(const void* x_perm, const int32_t* offsets, int64_t A_max, int32_t E, int64_t h,
+                            int64_t f, moe_act act, moe_dtype dt, const void* packed, const void* y_perm,
+                            moe_dtype ydt, const void* ws, size_t ws_bytes) {
     if (!valid_dtype(dt) || !valid_dtype(ydt) || !valid_act(act) || !valid_h(h) || E < 1 || f < 1 || A_max < 0)
         return MOE_ERR_INVALID_ARG;
     if (E > MOE_MAX_EXPERTS) return MOE_ERR_UNSUPPORTED;
@@ -142,6 +142,14 @@ moe_status moe_expert_ffn_shard(const void* x_perm, const int32_t* offsets, int6
         !ok_ptr(ws, any))
         return MOE_ERR_INVALID_ARG;
     if (ws_bytes < moe_ffn_workspace_size(A_max, E, h, f, act, dt)) return MOE_ERR_WORKSPACE;
+    return MOE_OK;
+}
+
+moe_status moe_expert_ffn_shard(const void* x_perm, const int32_t* offsets, int64_t A_max, int32_t E, int64_t h,
+                                int64_t f, moe_act act, moe_dtype dt, const void* packed, void* y_perm,
+                                moe_dtype ydt, void* ws, size_t ws_bytes, hipStream_t stream) {
+    const moe_status st = ffn_check(x_perm, offsets, A_max, E, h, f, act, dt, packed, y_perm, ydt, ws, ws_bytes);
+    if (st != MOE_OK) return st;
     const size_t mb = packed_matrix_bytes(E, h, f, dt);
     const unsigned char* base = static_cast<const unsigned char*>(packed);
     const bool swiglu = act == MOE_ACT_SWIGLU;
@@ -151,6 +159,26 @@ moe_status moe_expert_ffn_shard(const void* x_perm, const int32_t* offsets, int6
     return from_hip(moe::launch_ffn(x_perm, offsets, A_max, E, static_cast<int>(h), moe_padded_inner_width(f),
                                     static_cast<int>(act), dt == MOE_BF16, w1t, w3t, w2t, y_perm, ydt == MOE_BF16,
                                     ws, stream));
+}
+
+moe_status moe_expert_ffn_shard_per_expert(const void* x_perm, const int32_t* offsets, const int32_t* offsets_host,
+                                           int64_t A_max, int32_t E, int64_t h, int64_t f, moe_act act,
+                                           moe_dtype dt, const void* packed, void* y_perm, moe_dtype ydt, void* ws,
+                                           size_t ws_bytes, hipStream_t stream) {
+    const moe_status st = ffn_check(x_perm, offsets, A_max, E, h, f, act, dt, packed, y_perm, ydt, ws, ws_bytes);
+    if (st != MOE_OK) return st;
+    if (!offsets_host || offsets_host[0] < 0 || offsets_host[E] > A_max) return MOE_ERR_INVALID_ARG;
+    for (int32_t e = 0; e < E; ++e)
+        if (offsets_host[e + 1] < offsets_host[e]) return MOE_ERR_INVALID_ARG;
+    const size_t mb = packed_matrix_bytes(E, h, f, dt);
+    const unsigned char* base = static_cast<const unsigned char*>(packed);
+    const bool swiglu = act == MOE_ACT_SWIGLU;
+    const void* w1t = base;
+    const void* w3t = swiglu ? base + mb : nullptr;
+    const void* w2t = base + (swiglu ? 2 : 1) * mb;
+    return from_hip(moe::launch_ffn_per_expert(x_perm, offsets, offsets_host, A_max, E, static_cast<int>(h),
+                                               moe_padded_inner_width(f), static_cast<int>(act), dt == MOE_BF16, w1t,
+                                               w3t, w2t, y_perm, ydt == MOE_BF16, ws, stream));
 }
 
 moe_status moe_combine(const void* y_perm, moe_dtype ydt, const int32_t* pos_of, const float* topk_w, int64_t T,

@@ -860,12 +860,12 @@ hipError_t gemm1(bool bf16, GroupedGemm g, int64_t A_max, hipStream_t s) {
     return bf16 ? run_bf16_best<EPI, true>(g, A_max, s) : run_f32<EPI, false>(g, A_max, s);
 }
 
-}  // namespace
-
-hipError_t launch_ffn(const void* x_perm, const int32_t* offsets, int64_t A_max, int E, int h,
-                      int64_t fp, int act, bool bf16, const void* w1t, const void* w3t,
-                      const void* w2t, void* y_perm, bool y_bf16, void* hbuf, hipStream_t s) {
-    if (A_max == 0) return hipSuccess;
+// Both matmuls of the expert step.  grid_rows sizes the launches (an upper bound of the
+// rows the offsets describe); rows_max is the row count of x_perm, H and y_perm.
+hipError_t ffn_pair(const void* x_perm, const int32_t* offsets, int64_t grid_rows, int64_t rows_max, int E,
+                    int h, int64_t fp, int act, bool bf16, const void* w1t, const void* w3t, const void* w2t,
+                    void* y_perm, bool y_bf16, void* hbuf, hipStream_t s) {
+    if (grid_rows == 0) return hipSuccess;
     GroupedGemm g1{};
     g1.a = x_perm;
     g1.b = w1t;
@@ -877,11 +877,11 @@ hipError_t launch_ffn(const void* x_perm, const int32_t* offsets, int64_t A_max,
     g1.N = static_cast<int>(fp);
     g1.ldc = static_cast<int>(fp);
     g1.b_estride = fp * h;
-    g1.rows_max = A_max;
+    g1.rows_max = rows_max;
     hipError_t err;
-    if (act == MOE_ACT_SWIGLU) err = gemm1<kEpiSwiglu>(bf16, g1, A_max, s);
-    else if (act == MOE_ACT_GELU_TANH) err = gemm1<kEpiGeluTanh>(bf16, g1, A_max, s);
-    else err = gemm1<kEpiGelu>(bf16, g1, A_max, s);
+    if (act == MOE_ACT_SWIGLU) err = gemm1<kEpiSwiglu>(bf16, g1, grid_rows, s);
+    else if (act == MOE_ACT_GELU_TANH) err = gemm1<kEpiGeluTanh>(bf16, g1, grid_rows, s);
+    else err = gemm1<kEpiGelu>(bf16, g1, grid_rows, s);
     if (err != hipSuccess) return err;
 
     GroupedGemm g2{};
@@ -895,9 +895,40 @@ hipError_t launch_ffn(const void* x_perm, const int32_t* offsets, int64_t A_max,
     g2.N = h;
     g2.ldc = h;
     g2.b_estride = static_cast<int64_t>(h) * fp;
-    g2.rows_max = A_max;
-    if (bf16) return y_bf16 ? run_bf16_best<kEpiNone, true>(g2, A_max, s) : run_bf16_best<kEpiNone, false>(g2, A_max, s);
-    return y_bf16 ? run_f32<kEpiNone, true>(g2, A_max, s) : run_f32<kEpiNone, false>(g2, A_max, s);
+    g2.rows_max = rows_max;
+    if (bf16)
+        return y_bf16 ? run_bf16_best<kEpiNone, true>(g2, grid_rows, s) : run_bf16_best<kEpiNone, false>(g2, grid_rows, s);
+    return y_bf16 ? run_f32<kEpiNone, true>(g2, grid_rows, s) : run_f32<kEpiNone, false>(g2, grid_rows, s);
+}
+
+}  // namespace
+
+hipError_t launch_ffn(const void* x_perm, const int32_t* offsets, int64_t A_max, int E, int h,
+                      int64_t fp, int act, bool bf16, const void* w1t, const void* w3t,
+                      const void* w2t, void* y_perm, bool y_bf16, void* hbuf, hipStream_t s) {
+    return ffn_pair(x_perm, offsets, A_max, A_max, E, h, fp, act, bf16, w1t, w3t, w2t, y_perm, y_bf16, hbuf, s);
+}
+
+// One expert at a time: expert e's segment is the one-expert grouping (offsets + e), its
+// weights start e matrices into each packed block, and the launches are sized by its own
+// row count, read from the host copy of the offsets.
+hipError_t launch_ffn_per_expert(const void* x_perm, const int32_t* offsets, const int32_t* offsets_host,
+                                 int64_t A_max, int E, int h, int64_t fp, int act, bool bf16, const void* w1t,
+                                 const void* w3t, const void* w2t, void* y_perm, bool y_bf16, void* hbuf,
+                                 hipStream_t s) {
+    const int64_t es = bf16 ? 2 : 4;
+    const int64_t mat = fp * h * es;  // bytes of one expert's matrix in each packed block
+    for (int e = 0; e < E; ++e) {
+        const int64_t count = static_cast<int64_t>(offsets_host[e + 1]) - offsets_host[e];
+        if (count <= 0) continue;
+        const unsigned char* b1 = static_cast<const unsigned char*>(w1t) + e * mat;
+        const unsigned char* b3 = w3t ? static_cast<const unsigned char*>(w3t) + e * mat : nullptr;
+        const unsigned char* b2 = static_cast<const unsigned char*>(w2t) + e * mat;
+        const hipError_t err = ffn_pair(x_perm, offsets + e, count, A_max, 1, h, fp, act, bf16, b1, b3, b2, y_perm,
+                                        y_bf16, hbuf, s);
+        if (err != hipSuccess) return err;
+    }
+    return hipSuccess;
 }
 
 }  // namespace moe

@@ -175,6 +175,36 @@ def expert_ffn_shard(x_perm: torch.Tensor, offsets: torch.Tensor, packed: Packed
     return out
 
 
+def expert_ffn_shard_per_expert(x_perm: torch.Tensor, offsets: torch.Tensor, packed: PackedShard,
+                                out_dtype: Optional[torch.dtype] = None, A_max: Optional[int] = None,
+                                out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                                offsets_host: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Step 4 as one launch pair per expert (the ablation of the grouped operation).  The
+    per-expert row counts come from a host copy of the offsets; without one, the offsets are
+    read back here (a synchronization, as the per-expert loop needs)."""
+    _dev(x_perm, "x_perm"), _dev(offsets, "offsets")
+    if x_perm.dtype != packed.dtype:
+        raise TypeError("x_perm must have the packed weights' dtype")
+    A = x_perm.shape[0]
+    A_max = A if A_max is None else A_max
+    if A_max > A:
+        raise ValueError("A_max exceeds the rows of x_perm")
+    if offsets_host is None:
+        offsets_host = offsets.to("cpu")
+    offsets_host = offsets_host.to(torch.int32).contiguous()
+    if offsets_host.device.type != "cpu" or offsets_host.numel() != packed.E + 1:
+        raise ValueError("offsets_host must be a host tensor of E + 1 offsets")
+    out_dtype = out_dtype or x_perm.dtype
+    if out is None:
+        out = torch.empty((A, packed.h), dtype=out_dtype, device=x_perm.device)
+    if ws is None:
+        ws = torch.empty(max(ffn_workspace_size(A_max, packed), 16), dtype=torch.uint8, device=x_perm.device)
+    _lib.call("moe_expert_ffn_shard_per_expert", _ptr(x_perm), _ptr(offsets), offsets_host.data_ptr(), A_max,
+              packed.E, packed.h, packed.f, _lib.ACTS[packed.act], _DT[packed.dtype], _ptr(packed.buf), _ptr(out),
+              _dt(out), _ptr(ws), ws.numel(), _stream(x_perm, stream))
+    return out
+
+
 def combine(y_perm: torch.Tensor, pos_of: torch.Tensor, topk_w: torch.Tensor,
             out_dtype: Optional[torch.dtype] = None, out: Optional[torch.Tensor] = None,
             stream=None) -> torch.Tensor:

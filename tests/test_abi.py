@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 10, names
+    assert len(names) == 11, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(_lib.SIGNATURES)
@@ -119,6 +119,26 @@ def test_ffn_and_combine_reject_bad_arguments(lib):
     assert lib.moe_combine(A16, _lib.MOE_BF16, A16, A16, 4, 0, 64, A16, _lib.MOE_BF16, None) == _lib.MOE_ERR_INVALID_ARG
     assert lib.moe_combine(A16, _lib.MOE_BF16, A16, A16, 4, 1, 12, A16, _lib.MOE_BF16, None) == _lib.MOE_ERR_INVALID_ARG
     assert lib.moe_combine(None, _lib.MOE_BF16, None, None, 0, 1, 64, None, _lib.MOE_BF16, None) == _lib.MOE_OK
+
+
+def test_per_expert_ffn_rejects_bad_host_offsets(lib):
+    """The per-expert variant checks its host copy of the offsets before any launch."""
+    E = 4
+    ws = lib.moe_ffn_workspace_size(64, E, 64, 32, _lib.MOE_ACT_GELU, _lib.MOE_BF16)
+
+    def call(offs):
+        host = None if offs is None else (ctypes.c_int32 * len(offs))(*offs)
+        addr = None if host is None else ctypes.addressof(host)
+        return lib.moe_expert_ffn_shard_per_expert(A16, A16, addr, 64, E, 64, 32, _lib.MOE_ACT_GELU, _lib.MOE_BF16,
+                                                   A16, A16, _lib.MOE_BF16, A16, ws, None)
+
+    assert call(None) == _lib.MOE_ERR_INVALID_ARG
+    assert call([0, 10, 5, 20, 30]) == _lib.MOE_ERR_INVALID_ARG   # decreasing
+    assert call([-1, 10, 20, 30, 40]) == _lib.MOE_ERR_INVALID_ARG  # negative start
+    assert call([0, 10, 20, 30, 65]) == _lib.MOE_ERR_INVALID_ARG   # past A_max
+    bad_ws = lib.moe_expert_ffn_shard_per_expert(A16, A16, None, 64, E, 64, 32, _lib.MOE_ACT_GELU, _lib.MOE_BF16,
+                                                 A16, A16, _lib.MOE_BF16, A16, ws - 1, None)
+    assert bad_ws == _lib.MOE_ERR_WORKSPACE
 
 
 def test_python_binding_refuses_cpu_tensors():
