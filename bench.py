@@ -35,7 +35,8 @@ import synth  # noqa: E402
 PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_F32_TFLOPS = 157.3
-FFN_SOURCES = ["paper_2503_08467_amd/csrc/ffn.hip", "paper_2503_08467_amd/csrc/common.h"]
+FFN_SOURCES = ["paper_2503_08467_amd/csrc/ffn.hip", "paper_2503_08467_amd/csrc/common.h",
+               "paper_2503_08467_amd/csrc/lds_dma.h"]
 
 
 def ffn_source_hash() -> str:
