@@ -197,6 +197,8 @@ def main():
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run an untimed plain copy of this size first (counter calibration)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--unfused-gather", action="store_true",
+                    help="write x_perm in the dispatch step instead of gathering rows in the expert step")
     ap.add_argument("--ablation", action="store_true",
                     help="grouped launch vs one launch pair per expert over E = 8 .. 256 (paper's shape)")
     args = ap.parse_args()
@@ -223,7 +225,8 @@ def main():
     x, wg = to(L.x), to(L.wg)
     bias = to(L.sel_bias, torch.float32)
     packed = moe.pack_weights(to(L.w1), to(L.w2), to(L.w3), act=cfg.act)
-    layer = moe.MoEShardLayer(wg, packed, cfg.k, bool(cfg.renorm), max_tokens=cfg.T)
+    layer = moe.MoEShardLayer(wg, packed, cfg.k, bool(cfg.renorm), max_tokens=cfg.T,
+                              fused_gather=not args.unfused_gather)
     del L.w1, L.w2, L.w3
 
     stream = torch.cuda.current_stream(dev)
@@ -245,8 +248,12 @@ def main():
         moe.dispatch(layer.idx, x, cfg.E, out=layer.disp, ws=layer.dws)
         if ev: ev[2].record(stream)
         if ffn_ev: ffn_ev[0].record(stream)
-        moe.expert_ffn_shard(layer.disp.x_perm, layer.disp.offsets, packed, A_max=T * k, out=layer.y_perm,
-                             ws=layer.fws)
+        if layer.disp.x_perm is None:  # the expert step gathers the rows (no x_perm round trip)
+            moe.expert_ffn_shard_gather(x, layer.disp.row_src, layer.disp.offsets, packed, A_max=T * k,
+                                        out=layer.y_perm, ws=layer.fws)
+        else:
+            moe.expert_ffn_shard(layer.disp.x_perm, layer.disp.offsets, packed, A_max=T * k, out=layer.y_perm,
+                                 ws=layer.fws)
         if ffn_ev: ffn_ev[1].record(stream)
         if ev: ev[3].record(stream)
         moe.combine(layer.y_perm, layer.disp.pos_of, layer.w, out=layer.y)
@@ -294,7 +301,8 @@ def main():
             {"bound": "mfma", "achieved": round(achieved_tflops, 1), "peak": peak_tf, "unit": "TFLOP/s",
              "frac": round(achieved_tflops / peak_tf, 4)})
     roof["traffic"] = measured_traffic(args.config)
-    roof["kernel"] = "moe_expert_ffn_shard (grouped GEMM1+act and GEMM2, one launch each)"
+    roof["kernel"] = ("moe_expert_ffn_shard" + ("" if args.unfused_gather else "_gather") +
+                      " (grouped GEMM1+act and GEMM2, one launch each)")
     roof["algorithmic"] = {"bytes": ffn_bytes, "flops": ffn_flops, "touched_experts": touched,
                            "mfma_util": round(achieved_tflops / peak_tf, 4),
                            "hbm_frac": round(achieved_gbs / PEAK_HBM_GBS, 4)}

@@ -94,7 +94,9 @@ size_t moe_dispatch_workspace_size(int64_t T, int32_t k, int32_t E);
  *             is valid
  *   row_src   [A]   out: token of the assignment at grouped position p
  *   pos_of    [T,k] out: grouped position of assignment (t, j)
- *   x_perm    [A, h] out: x_perm[p] = x[row_src[p]], bit copies
+ *   x_perm    [A, h] out: x_perm[p] = x[row_src[p]], bit copies; may be NULL, and then
+ *             only the indices are written (x is not read; moe_expert_ffn_shard_gather
+ *             reads the rows through row_src instead)
  *   ws        moe_dispatch_workspace_size(T, k, E) bytes, 16-byte aligned
  * T == 0 writes zero counts and offsets. */
 moe_status moe_dispatch(const int32_t *topk_idx, int64_t T, int32_t k, int32_t E,
@@ -147,6 +149,20 @@ moe_status moe_expert_ffn_shard(const void *x_perm, const int32_t *offsets, int6
                                 int32_t E, int64_t h, int64_t f, moe_act act, moe_dtype dt,
                                 const void *packed, void *y_perm, moe_dtype ydt, void *ws,
                                 size_t ws_bytes, hipStream_t stream);
+
+/* Step 4 with Step 2's row gather folded into it (Section 3.3's concatenation of an
+ * expert's tokens done by the loads of the first matmul): the same result as
+ * moe_expert_ffn_shard on x_perm[p] = x[row_src[p]], bit for bit, without x_perm.
+ *   x        [T, h] dtype dt, the unpermuted rows; T * h * sizeof(dt) < 4 GiB
+ *            (else MOE_ERR_UNSUPPORTED)
+ *   row_src  [A_max] int32 from moe_dispatch (entries past offsets[E] are never used as
+ *            more than a clamped row index)
+ *   other arguments as moe_expert_ffn_shard. */
+moe_status moe_expert_ffn_shard_gather(const void *x, int64_t T, const int32_t *row_src,
+                                       const int32_t *offsets, int64_t A_max, int32_t E,
+                                       int64_t h, int64_t f, moe_act act, moe_dtype dt,
+                                       const void *packed, void *y_perm, moe_dtype ydt, void *ws,
+                                       size_t ws_bytes, hipStream_t stream);
 
 /* Ablation of the single grouped operation (Section 3.3's second optimization, the one the
  * paper's ablation study removes): the same result as moe_expert_ffn_shard, bit for bit,

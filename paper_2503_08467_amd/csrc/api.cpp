@@ -77,8 +77,11 @@ moe_status moe_dispatch(const int32_t* topk_idx, int64_t T, int32_t k, int32_t E
     if (E > MOE_MAX_EXPERTS) return MOE_ERR_UNSUPPORTED;
     if (T * k >= INT32_MAX) return MOE_ERR_INVALID_ARG;
     const bool any = T > 0;
-    if (!ok_ptr(topk_idx, any) || !ok_ptr(x, any) || !ok_ptr(counts, true) || !ok_ptr(offsets, true) ||
-        !ok_ptr(row_src, any) || !ok_ptr(pos_of, any) || !ok_ptr(x_perm, any) || !ok_ptr(ws, true))
+    // x_perm may be NULL: the grouped rows are then not written (moe_expert_ffn_shard_gather
+    // reads them through row_src); x is only read when x_perm is given
+    const bool gather = x_perm != nullptr;
+    if (!ok_ptr(topk_idx, any) || !ok_ptr(x, any && gather) || !ok_ptr(counts, true) || !ok_ptr(offsets, true) ||
+        !ok_ptr(row_src, any) || !ok_ptr(pos_of, any) || (x_perm && !aligned16(x_perm)) || !ok_ptr(ws, true))
         return MOE_ERR_INVALID_ARG;
     if (ws_bytes < moe_dispatch_workspace_size(T, k, E)) return MOE_ERR_WORKSPACE;
     return from_hip(moe::launch_dispatch(topk_idx, T, k, E, x, elem_bytes(xdt), static_cast<int>(h), counts,
@@ -159,6 +162,26 @@ moe_status moe_expert_ffn_shard(const void* x_perm, const int32_t* offsets, int6
     return from_hip(moe::launch_ffn(x_perm, offsets, A_max, E, static_cast<int>(h), moe_padded_inner_width(f),
                                     static_cast<int>(act), dt == MOE_BF16, w1t, w3t, w2t, y_perm, ydt == MOE_BF16,
                                     ws, stream));
+}
+
+moe_status moe_expert_ffn_shard_gather(const void* x, int64_t T, const int32_t* row_src, const int32_t* offsets,
+                                       int64_t A_max, int32_t E, int64_t h, int64_t f, moe_act act, moe_dtype dt,
+                                       const void* packed, void* y_perm, moe_dtype ydt, void* ws, size_t ws_bytes,
+                                       hipStream_t stream) {
+    const moe_status st = ffn_check(x, offsets, A_max, E, h, f, act, dt, packed, y_perm, ydt, ws, ws_bytes);
+    if (st != MOE_OK) return st;
+    if (T < 0 || (A_max > 0 && (T < 1 || !ok_ptr(row_src, true)))) return MOE_ERR_INVALID_ARG;
+    // a source row's byte offset must fit the kernels' 32-bit per-lane offsets
+    if (T * h * elem_bytes(dt) >= (int64_t(1) << 32)) return MOE_ERR_UNSUPPORTED;
+    const size_t mb = packed_matrix_bytes(E, h, f, dt);
+    const unsigned char* base = static_cast<const unsigned char*>(packed);
+    const bool swiglu = act == MOE_ACT_SWIGLU;
+    const void* w1t = base;
+    const void* w3t = swiglu ? base + mb : nullptr;
+    const void* w2t = base + (swiglu ? 2 : 1) * mb;
+    return from_hip(moe::launch_ffn_gather(x, T, row_src, offsets, A_max, E, static_cast<int>(h),
+                                           moe_padded_inner_width(f), static_cast<int>(act), dt == MOE_BF16, w1t, w3t,
+                                           w2t, y_perm, ydt == MOE_BF16, ws, stream));
 }
 
 moe_status moe_expert_ffn_shard_per_expert(const void* x_perm, const int32_t* offsets, const int32_t* offsets_host,

@@ -184,11 +184,13 @@ hipError_t launch_dispatch(const int32_t* idx, int64_t T, int k, int E, const vo
     if (nchunks > 0) {
         hipLaunchKernelGGL(dispatch_rank, dim3(nchunks), dim3(kDispThreads), 0, s, idx, A, k, E, nbits,
                            nchunks, base, row_src, pos_of);
-        const uint32_t nvec = static_cast<uint32_t>(static_cast<int64_t>(h) * elem_bytes / 16);
-        const int64_t blocks = ceil_div(A, 4 * kGatherRows);
-        hipLaunchKernelGGL(dispatch_gather, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
-                           static_cast<const uint4*>(x), row_src, offsets, E, static_cast<uint32_t>(A),
-                           static_cast<uint32_t>(T), nvec, static_cast<uint4*>(x_perm));
+        if (x_perm) {  // without x_perm the expert step gathers the rows itself
+            const uint32_t nvec = static_cast<uint32_t>(static_cast<int64_t>(h) * elem_bytes / 16);
+            const int64_t blocks = ceil_div(A, 4 * kGatherRows);
+            hipLaunchKernelGGL(dispatch_gather, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
+                               static_cast<const uint4*>(x), row_src, offsets, E, static_cast<uint32_t>(A),
+                               static_cast<uint32_t>(T), nvec, static_cast<uint4*>(x_perm));
+        }
     }
     return hipGetLastError();
 }

@@ -31,7 +31,7 @@ namespace {
 enum Epi { kEpiGelu = 0, kEpiGeluTanh = 1, kEpiSwiglu = 2, kEpiNone = 3 };
 
 struct GroupedGemm {
-    const void* a;           // [rows][K]
+    const void* a;           // [rows][K], or with `gather` [a_rows][K] read through it
     const void* b;           // [E][N rows][K]  (K-contiguous weights)
     const void* b2;          // SwiGLU up projection, same layout as b
     void* c;                 // [rows][ldc]
@@ -39,7 +39,19 @@ struct GroupedGemm {
     int E, K, N, ldc, n_tiles;
     int64_t b_estride;  // elements from one expert's weights to the next
     int64_t rows_max;   // rows of a and c; no row at or past it is touched
+    // Up-projection only: grouped row p reads row gather[p] of a (clamped to
+    // [0, a_rows)) instead of row p -- the dispatch gather folded into the loads.
+    const int32_t* gather;
+    int64_t a_rows;
 };
+
+// Source row of grouped row p: p itself, or gather[p] clamped into a (entries past the
+// assigned rows are never written by the dispatch, so their value is arbitrary).
+__device__ __forceinline__ int64_t source_row(const GroupedGemm& g, int64_t p) {
+    if (!g.gather) return p;
+    const int64_t r = g.gather[p];
+    return r < 0 ? 0 : (r >= g.a_rows ? g.a_rows - 1 : r);
+}
 
 constexpr int kThreads = 256;
 
@@ -167,7 +179,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16(GroupedGemm g) {
             const int row = v >> 3, kc = (v & 7) * 8;
             const int64_t ar = row0 + row;
             ra[i] = (ar < row_end && k0 + kc < g.K)
-                        ? *reinterpret_cast<const uint4*>(A + ar * g.K + k0 + kc)
+                        ? *reinterpret_cast<const uint4*>(A + source_row(g, ar) * g.K + k0 + kc)
                         : make_uint4(0, 0, 0, 0);
         }
 #pragma unroll
@@ -475,7 +487,22 @@ void gemm_bf16_lds(GroupedGemm g) {
     auto set_tile = [&](int L) {
         const TileGeom t = tile_geom<BM, BN>(g, tstart, total_m, L);
         const int64_t rb = kUp ? 2 * static_cast<int64_t>(g.K) : 64;
-        src_a = uniform_ptr(static_cast<const unsigned char*>(g.a) + t.row_base * rb);
+        if (kUp && g.gather) {
+            // this lane's activation rows come from the gathered source rows (the index
+            // load makes the compiler wait for the loads in flight: once per tile)
+            const int r_lane = lane / CPR, c_lane = lane % CPR;
+            const int a_lim = static_cast<int>(g.rows_max < BM ? g.rows_max : BM) - 1;
+#pragma unroll
+            for (int j = 0; j < kAJ; ++j) {
+                const int R = (j * 4 + wave) * RPI + r_lane;
+                const int kc = c_lane ^ ((R >> SH) & (CPR - 1));
+                const int64_t src = source_row(g, t.row_base + min(R, a_lim));
+                voff[j] = static_cast<uint32_t>(src) * static_cast<uint32_t>(2 * g.K) + static_cast<uint32_t>(kc * 16);
+            }
+            src_a = uniform_ptr(g.a);
+        } else {
+            src_a = uniform_ptr(static_cast<const unsigned char*>(g.a) + t.row_base * rb);
+        }
         const int64_t boff = (t.e * g.b_estride) * 2 + static_cast<int64_t>(t.n_base) * 64;
         src_b0 = uniform_ptr(static_cast<const unsigned char*>(g.b) + boff);
         src_b1 = NB > 1 ? uniform_ptr(static_cast<const unsigned char*>(g.b2) + boff) : src_b0;
@@ -652,7 +679,7 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GroupedGemm g) {
     for (int k0 = 0; k0 < g.K; k0 += kFBK) {
         const bool kv = k0 + lk < g.K;
         const int64_t ar = row0 + lrow;
-        const float4 a = (ar < row_end && kv) ? *reinterpret_cast<const float4*>(A + ar * g.K + k0 + lk)
+        const float4 a = (ar < row_end && kv) ? *reinterpret_cast<const float4*>(A + source_row(g, ar) * g.K + k0 + lk)
                                               : make_float4(0.f, 0.f, 0.f, 0.f);
         As[lk + 0][lrow] = a.x;
         As[lk + 1][lrow] = a.y;
@@ -797,10 +824,13 @@ hipError_t gemm1(bool bf16, GroupedGemm g, int64_t A_max, hipStream_t s) {
 // rows the offsets describe); rows_max is the row count of x_perm, H and y_perm.
 hipError_t ffn_pair(const void* x_perm, const int32_t* offsets, int64_t grid_rows, int64_t rows_max, int E,
                     int h, int64_t fp, int act, bool bf16, const void* w1t, const void* w3t, const void* w2t,
-                    void* y_perm, bool y_bf16, void* hbuf, hipStream_t s) {
+                    void* y_perm, bool y_bf16, void* hbuf, hipStream_t s, const int32_t* gather = nullptr,
+                    int64_t a_rows = 0) {
     if (grid_rows == 0) return hipSuccess;
     GroupedGemm g1{};
     g1.a = x_perm;
+    g1.gather = gather;
+    g1.a_rows = a_rows;
     g1.b = w1t;
     g1.b2 = w3t;
     g1.c = hbuf;
@@ -840,6 +870,12 @@ hipError_t launch_ffn(const void* x_perm, const int32_t* offsets, int64_t A_max,
                       int64_t fp, int act, bool bf16, const void* w1t, const void* w3t,
                       const void* w2t, void* y_perm, bool y_bf16, void* hbuf, hipStream_t s) {
     return ffn_pair(x_perm, offsets, A_max, A_max, E, h, fp, act, bf16, w1t, w3t, w2t, y_perm, y_bf16, hbuf, s);
+}
+
+hipError_t launch_ffn_gather(const void* x, int64_t T, const int32_t* row_src, const int32_t* offsets, int64_t A_max,
+                             int E, int h, int64_t fp, int act, bool bf16, const void* w1t, const void* w3t,
+                             const void* w2t, void* y_perm, bool y_bf16, void* hbuf, hipStream_t s) {
+    return ffn_pair(x, offsets, A_max, A_max, E, h, fp, act, bf16, w1t, w3t, w2t, y_perm, y_bf16, hbuf, s, row_src, T);
 }
 
 // One expert at a time: expert e's segment is the one-expert grouping (offsets + e), its

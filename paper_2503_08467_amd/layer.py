@@ -76,34 +76,35 @@ class Dispatch:
     offsets: torch.Tensor  # [E+1] int32
     row_src: torch.Tensor  # [A] int32
     pos_of: torch.Tensor  # [T,k] int32
-    x_perm: torch.Tensor  # [A,h]
+    x_perm: Optional[torch.Tensor]  # [A,h]; None when the expert step gathers the rows itself
 
 
 def dispatch_workspace_size(T: int, k: int, E: int) -> int:
     return int(_lib.load().moe_dispatch_workspace_size(T, k, E))
 
 
-def alloc_dispatch(T: int, k: int, E: int, h: int, dtype, device) -> tuple:
-    """Output buffers and workspace of moe_dispatch."""
+def alloc_dispatch(T: int, k: int, E: int, h: int, dtype, device, x_perm: bool = True) -> tuple:
+    """Output buffers and workspace of moe_dispatch (x_perm=False: indices only)."""
     d = Dispatch(counts=torch.empty(E, dtype=torch.int32, device=device),
                  offsets=torch.empty(E + 1, dtype=torch.int32, device=device),
                  row_src=torch.empty(T * k, dtype=torch.int32, device=device),
                  pos_of=torch.empty((T, k), dtype=torch.int32, device=device),
-                 x_perm=torch.empty((T * k, h), dtype=dtype, device=device))
+                 x_perm=torch.empty((T * k, h), dtype=dtype, device=device) if x_perm else None)
     ws = torch.empty(max(dispatch_workspace_size(T, k, E), 16), dtype=torch.uint8, device=device)
     return d, ws
 
 
 def dispatch(topk_idx: torch.Tensor, x: torch.Tensor, E: int, out: Optional[Dispatch] = None,
-             ws: Optional[torch.Tensor] = None, stream=None) -> Dispatch:
-    """Step 2: group the T*k assignments per expert (stable in (t, j) order)."""
+             ws: Optional[torch.Tensor] = None, stream=None, x_perm: bool = True) -> Dispatch:
+    """Step 2: group the T*k assignments per expert (stable in (t, j) order).  With
+    x_perm=False (or out.x_perm None) only the indices are written."""
     _dev(topk_idx, "topk_idx"), _dev(x, "x")
     if topk_idx.dtype != torch.int32:
         raise TypeError("topk_idx must be int32")
     T, k = topk_idx.shape
     h = x.shape[1]
     if out is None or ws is None:
-        out, ws = alloc_dispatch(T, k, E, h, x.dtype, x.device)
+        out, ws = alloc_dispatch(T, k, E, h, x.dtype, x.device, x_perm=x_perm)
     _lib.call("moe_dispatch", _ptr(topk_idx), T, k, E, _ptr(x), _dt(x), h, _ptr(out.counts),
               _ptr(out.offsets), _ptr(out.row_src), _ptr(out.pos_of), _ptr(out.x_perm), _ptr(ws),
               ws.numel(), _stream(x, stream))
@@ -175,6 +176,32 @@ def expert_ffn_shard(x_perm: torch.Tensor, offsets: torch.Tensor, packed: Packed
     return out
 
 
+def expert_ffn_shard_gather(x: torch.Tensor, row_src: torch.Tensor, offsets: torch.Tensor, packed: PackedShard,
+                            out_dtype: Optional[torch.dtype] = None, A_max: Optional[int] = None,
+                            out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                            stream=None) -> torch.Tensor:
+    """Step 4 reading grouped row p from x[row_src[p]] (the dispatch gather folded in)."""
+    _dev(x, "x"), _dev(row_src, "row_src"), _dev(offsets, "offsets")
+    if x.dtype != packed.dtype:
+        raise TypeError("x must have the packed weights' dtype")
+    if row_src.dtype != torch.int32:
+        raise TypeError("row_src must be int32")
+    T = x.shape[0]
+    A = row_src.shape[0]
+    A_max = A if A_max is None else A_max
+    if A_max > A:
+        raise ValueError("A_max exceeds the rows of row_src")
+    out_dtype = out_dtype or x.dtype
+    if out is None:
+        out = torch.empty((A, packed.h), dtype=out_dtype, device=x.device)
+    if ws is None:
+        ws = torch.empty(max(ffn_workspace_size(A_max, packed), 16), dtype=torch.uint8, device=x.device)
+    _lib.call("moe_expert_ffn_shard_gather", _ptr(x), T, _ptr(row_src), _ptr(offsets), A_max, packed.E, packed.h,
+              packed.f, _lib.ACTS[packed.act], _DT[packed.dtype], _ptr(packed.buf), _ptr(out), _dt(out), _ptr(ws),
+              ws.numel(), _stream(x, stream))
+    return out
+
+
 def expert_ffn_shard_per_expert(x_perm: torch.Tensor, offsets: torch.Tensor, packed: PackedShard,
                                 out_dtype: Optional[torch.dtype] = None, A_max: Optional[int] = None,
                                 out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
@@ -228,7 +255,7 @@ class MoEShardLayer:
 
     def __init__(self, w_gate: torch.Tensor, packed: PackedShard, k: int, renorm: bool = False,
                  max_tokens: int = 0, out_dtype: Optional[torch.dtype] = None,
-                 partial_dtype: Optional[torch.dtype] = None):
+                 partial_dtype: Optional[torch.dtype] = None, fused_gather: bool = True):
         self.w_gate = _dev(w_gate, "w_gate")
         self.packed = packed
         self.E, self.h = w_gate.shape
@@ -236,6 +263,8 @@ class MoEShardLayer:
         self.renorm = renorm
         self.out_dtype = out_dtype or w_gate.dtype
         self.partial_dtype = partial_dtype or w_gate.dtype
+        # fold the dispatch row gather into the expert step (no x_perm buffer)
+        self.fused_gather = fused_gather
         self._cap = 0
         if max_tokens:
             self._alloc(max_tokens)
@@ -245,7 +274,7 @@ class MoEShardLayer:
         k, E, h = self.k, self.E, self.h
         self.idx = torch.empty((T, k), dtype=torch.int32, device=dev)
         self.w = torch.empty((T, k), dtype=torch.float32, device=dev)
-        self.disp, self.dws = alloc_dispatch(T, k, E, h, self.w_gate.dtype, dev)
+        self.disp, self.dws = alloc_dispatch(T, k, E, h, self.w_gate.dtype, dev, x_perm=not self.fused_gather)
         self.y_perm = torch.empty((T * k, h), dtype=self.partial_dtype, device=dev)
         self.fws = torch.empty(max(ffn_workspace_size(T * k, self.packed), 16), dtype=torch.uint8, device=dev)
         self.y = torch.empty((T, h), dtype=self.out_dtype, device=dev)
@@ -259,10 +288,14 @@ class MoEShardLayer:
         idx, w = self.idx[:T], self.w[:T]
         route(x, self.w_gate, k, sel_bias, self.renorm, out=(idx, w))
         d = Dispatch(self.disp.counts, self.disp.offsets, self.disp.row_src[:T * k], self.disp.pos_of[:T],
-                     self.disp.x_perm[:T * k])
+                     None if self.disp.x_perm is None else self.disp.x_perm[:T * k])
         dispatch(idx, x, self.E, out=d, ws=self.dws)
-        y_perm = expert_ffn_shard(d.x_perm, d.offsets, self.packed, A_max=T * k, out=self.y_perm[:T * k],
-                                  ws=self.fws)
+        if d.x_perm is None:
+            y_perm = expert_ffn_shard_gather(x, d.row_src, d.offsets, self.packed, A_max=T * k,
+                                             out=self.y_perm[:T * k], ws=self.fws)
+        else:
+            y_perm = expert_ffn_shard(d.x_perm, d.offsets, self.packed, A_max=T * k, out=self.y_perm[:T * k],
+                                      ws=self.fws)
         y = combine(y_perm, d.pos_of, w, out=self.y[:T])
         self.last = dict(idx=idx, w=w, dispatch=d, y_perm=y_perm)
         return y

@@ -216,6 +216,41 @@ def test_per_expert_launches_match_grouped(dtype, act, counts, h, f):
     assert rowwise(np_of(y_each), ref) <= TOL[dtype]
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("act", ["gelu", "swiglu"])
+@pytest.mark.parametrize("T,k,E,h,f", [(700, 2, 6, 256, 200), (90, 1, 3, 72, 128), (1500, 1, 4, 768, 384)])
+def test_gathered_rows_match_x_perm(dtype, act, T, k, E, h, f):
+    """The expert step reading x[row_src[p]] itself equals the one reading x_perm, bit for
+    bit; some ids are invalid (dropped), so row_src has unwritten entries past offsets[E]."""
+    rng = np.random.default_rng(T + h)
+    x = rng.standard_normal((T, h)).astype(np.float32)
+    w1 = (rng.standard_normal((E, h, f)) * 0.05).astype(np.float32)
+    w3 = (rng.standard_normal((E, h, f)) * 0.05).astype(np.float32) if act == "swiglu" else None
+    w2 = (rng.standard_normal((E, f, h)) * 0.05).astype(np.float32)
+    if dtype == "bf16":
+        x, w1, w2 = synth.round_to_bf16(x), synth.round_to_bf16(w1), synth.round_to_bf16(w2)
+        w3 = None if w3 is None else synth.round_to_bf16(w3)
+    idx = np.stack([rng.permutation(E + 1)[:k] for _ in range(T)]).astype(np.int32)  # id E is invalid
+    dt = tdt(dtype)
+    xd = to_dev(x, dt)
+    packed = moe.pack_weights(to_dev(w1, dt), to_dev(w2, dt), to_dev(w3, dt), f=f, act=act)
+    d_full = moe.dispatch(to_dev(idx, torch.int32), xd, E)
+    d_idx = moe.dispatch(to_dev(idx, torch.int32), xd, E, x_perm=False)
+    d_idx.row_src.fill_(-123456)  # poison, then dispatch again: entries past offsets[E] stay poisoned
+    d_idx = moe.dispatch(to_dev(idx, torch.int32), xd, E, out=d_idx,
+                         ws=torch.empty(moe.dispatch_workspace_size(T, k, E), dtype=torch.uint8, device="cuda"))
+    y_perm = moe.expert_ffn_shard(d_full.x_perm, d_full.offsets, packed)
+    y_gath = moe.expert_ffn_shard_gather(xd, d_idx.row_src, d_idx.offsets, packed)
+    torch.cuda.synchronize()
+    n = int(d_full.offsets[-1].item())
+    assert n < T * k
+    ib = torch.int16 if dt == torch.bfloat16 else torch.int32
+    assert torch.equal(y_perm[:n].view(ib), y_gath[:n].view(ib))
+    offsets = d_full.offsets.cpu().numpy()
+    ref = oracle.expert_ffn(x[d_full.row_src.cpu().numpy()[:n]], offsets, w1, w3, w2, act)
+    assert rowwise(np_of(y_gath[:n]), ref) <= TOL[dtype]
+
+
 @pytest.mark.parametrize("g", [0, 1, 2, 3])
 def test_ffn_shard_slice_of_full_weights(g):
     """moe_pack_weights cuts shard g (inner columns [g*f, (g+1)*f)) out of the full weights;
@@ -269,12 +304,12 @@ def test_combine_parity(ydt, odt, T, k, h):
 
 # ------------------------------------------------------------------------------- whole layer
 
-def _gpu_layer(L, partial_dtype=None):
+def _gpu_layer(L, partial_dtype=None, fused_gather=True):
     cfg = L.cfg
     dt = tdt(cfg.dtype)
     packed = moe.pack_weights(to_dev(L.w1, dt), to_dev(L.w2, dt), to_dev(L.w3, dt), act=cfg.act)
     layer = moe.MoEShardLayer(to_dev(L.wg, dt), packed, cfg.k, bool(cfg.renorm), max_tokens=cfg.T,
-                              partial_dtype=partial_dtype)
+                              partial_dtype=partial_dtype, fused_gather=fused_gather)
     x = to_dev(L.x, dt)
     bias = to_dev(L.sel_bias, torch.float32)
     y = layer(x, bias)
@@ -285,11 +320,12 @@ def _gpu_layer(L, partial_dtype=None):
 SMALL = [("c1", None), ("c2", 1536), ("c3", 4096), ("c4", 160), ("c5", 600), ("c5dec", None)]
 
 
+@pytest.mark.parametrize("fused", [True, False])
 @pytest.mark.parametrize("name,T", SMALL)
-def test_layer_end_to_end(name, T):
+def test_layer_end_to_end(name, T, fused):
     L = synth.make(name, seed=0, **({"T": T} if T else {}))
     cfg = L.cfg
-    layer, x, bias, y = _gpu_layer(L)
+    layer, x, bias, y = _gpu_layer(L, fused_gather=fused)
     ref = oracle.forward(L)
     last = layer.last
     gi = last["idx"].cpu().numpy()
@@ -302,7 +338,8 @@ def test_layer_end_to_end(name, T):
         for key in ("counts", "offsets", "row_src"):
             assert np.array_equal(getattr(d, key).cpu().numpy(), ref[key]), key
         assert np.array_equal(by_expert(d.pos_of.cpu().numpy(), gi), by_expert(ref["pos_of"], ref["idx"]))
-        assert np.array_equal(np_of(d.x_perm), ref["x_perm"])
+        if d.x_perm is not None:
+            assert np.array_equal(np_of(d.x_perm), ref["x_perm"])
         assert rowwise(np_of(last["y_perm"]), ref["y_perm"]) <= tol
     else:
         print(f"{name}: {(~same_set).sum()} tokens picked a different but equally valid set")
