@@ -238,6 +238,8 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    top1_fused = cfg.k == 1 and not args.unfused_gather
+
     def step(ev=None, ffn_ev=None):
         """One layer forward.  ev: 5 events around the four calls (stage breakdown);
         ffn_ev: 2 events around the expert-FFN call only (kept in the timed loop)."""
@@ -248,7 +250,10 @@ def main():
         moe.dispatch(layer.idx, x, cfg.E, out=layer.disp, ws=layer.dws)
         if ev: ev[2].record(stream)
         if ffn_ev: ffn_ev[0].record(stream)
-        if layer.disp.x_perm is None:  # the expert step gathers the rows (no x_perm round trip)
+        if top1_fused:  # gather, expert step and the top-1 combine in one call
+            moe.expert_ffn_shard_top1(x, layer.disp.row_src, layer.w.view(-1), layer.disp.offsets, packed,
+                                      out=layer.y, ws=layer.fws)
+        elif layer.disp.x_perm is None:  # the expert step gathers the rows (no x_perm round trip)
             moe.expert_ffn_shard_gather(x, layer.disp.row_src, layer.disp.offsets, packed, A_max=T * k,
                                         out=layer.y_perm, ws=layer.fws)
         else:
@@ -256,7 +261,8 @@ def main():
                                  ws=layer.fws)
         if ffn_ev: ffn_ev[1].record(stream)
         if ev: ev[3].record(stream)
-        moe.combine(layer.y_perm, layer.disp.pos_of, layer.w, out=layer.y)
+        if not top1_fused:
+            moe.combine(layer.y_perm, layer.disp.pos_of, layer.w, out=layer.y)
         if ev: ev[4].record(stream)
 
     for _ in range(args.warmup):
@@ -301,7 +307,7 @@ def main():
             {"bound": "mfma", "achieved": round(achieved_tflops, 1), "peak": peak_tf, "unit": "TFLOP/s",
              "frac": round(achieved_tflops / peak_tf, 4)})
     roof["traffic"] = measured_traffic(args.config)
-    roof["kernel"] = ("moe_expert_ffn_shard" + ("" if args.unfused_gather else "_gather") +
+    roof["kernel"] = ("moe_expert_ffn_shard" + ("_top1" if top1_fused else "" if args.unfused_gather else "_gather") +
                       " (grouped GEMM1+act and GEMM2, one launch each)")
     roof["algorithmic"] = {"bytes": ffn_bytes, "flops": ffn_flops, "touched_experts": touched,
                            "mfma_util": round(achieved_tflops / peak_tf, 4),
@@ -326,7 +332,8 @@ def main():
                    "parallelism": "single device"},
         "stages_us": {"route": round(stage_us[0], 2), "dispatch": round(stage_us[1], 2),
                       "expert_ffn": round(stage_us[2], 2), "combine": round(stage_us[3], 2),
-                      "note": "separate untimed pass with events between calls"},
+                      "note": "separate untimed pass with events between calls" +
+                              ("; top-1: the combine is part of the expert step" if top1_fused else "")},
         "expert_ffn_us_timed": round(ffn_us, 2),
         "roofline": roof,
     }

@@ -164,6 +164,24 @@ moe_status moe_expert_ffn_shard_gather(const void *x, int64_t T, const int32_t *
                                        const void *packed, void *y_perm, moe_dtype ydt, void *ws,
                                        size_t ws_bytes, hipStream_t stream);
 
+/* Steps 4 and 5 together for top-1 routing (k = 1): the expert step reads its rows through
+ * row_src and its down-projection epilogue writes each token's gate-weighted result
+ * straight into y, so neither x_perm nor y_perm nor moe_combine is needed:
+ *     y[t] = topk_w[t] * (act(x[t] . W1_e^g) . W2_e^g),   e = the token's expert
+ * computed in fp32 and rounded once to out_dt.  A token whose pick was dropped (an id
+ * outside [0, E) in moe_dispatch) is not written.
+ *   x        [T, h] dtype dt; T * h * sizeof(dt) < 4 GiB (else MOE_ERR_UNSUPPORTED)
+ *   row_src  [T] int32 and offsets [E+1] from moe_dispatch with k = 1
+ *   topk_w   [T] fp32 gate weights from moe_route
+ *   y        [T, h] out, dtype out_dt
+ *   ws       moe_ffn_workspace_size(T, E, h, f, act, dt) bytes
+ *   other arguments as moe_expert_ffn_shard (A_max = T). */
+moe_status moe_expert_ffn_shard_top1(const void *x, int64_t T, const int32_t *row_src,
+                                     const float *topk_w, const int32_t *offsets, int32_t E,
+                                     int64_t h, int64_t f, moe_act act, moe_dtype dt,
+                                     const void *packed, void *y, moe_dtype out_dt, void *ws,
+                                     size_t ws_bytes, hipStream_t stream);
+
 /* Ablation of the single grouped operation (Section 3.3's second optimization, the one the
  * paper's ablation study removes): the same result as moe_expert_ffn_shard, bit for bit,
  * computed with one launch of each matmul per expert that has rows -- Step 4's per-expert

@@ -184,6 +184,26 @@ moe_status moe_expert_ffn_shard_gather(const void* x, int64_t T, const int32_t* 
                                            w2t, y_perm, ydt == MOE_BF16, ws, stream));
 }
 
+moe_status moe_expert_ffn_shard_top1(const void* x, int64_t T, const int32_t* row_src, const float* topk_w,
+                                     const int32_t* offsets, int32_t E, int64_t h, int64_t f, moe_act act, moe_dtype dt,
+                                     const void* packed, void* y, moe_dtype out_dt, void* ws, size_t ws_bytes,
+                                     hipStream_t stream) {
+    const moe_status st = ffn_check(x, offsets, T, E, h, f, act, dt, packed, y, out_dt, ws, ws_bytes);
+    if (st != MOE_OK) return st;
+    if (T > 0 && (!ok_ptr(row_src, true) || !topk_w || (reinterpret_cast<uintptr_t>(topk_w) & 3u)))
+        return MOE_ERR_INVALID_ARG;
+    if (T * h * elem_bytes(dt) >= (int64_t(1) << 32)) return MOE_ERR_UNSUPPORTED;
+    const size_t mb = packed_matrix_bytes(E, h, f, dt);
+    const unsigned char* base = static_cast<const unsigned char*>(packed);
+    const bool swiglu = act == MOE_ACT_SWIGLU;
+    const void* w1t = base;
+    const void* w3t = swiglu ? base + mb : nullptr;
+    const void* w2t = base + (swiglu ? 2 : 1) * mb;
+    return from_hip(moe::launch_ffn_top1(x, T, row_src, topk_w, offsets, T, E, static_cast<int>(h),
+                                         moe_padded_inner_width(f), static_cast<int>(act), dt == MOE_BF16, w1t, w3t,
+                                         w2t, y, out_dt == MOE_BF16, ws, stream));
+}
+
 moe_status moe_expert_ffn_shard_per_expert(const void* x_perm, const int32_t* offsets, const int32_t* offsets_host,
                                            int64_t A_max, int32_t E, int64_t h, int64_t f, moe_act act,
                                            moe_dtype dt, const void* packed, void* y_perm, moe_dtype ydt, void* ws,

@@ -43,6 +43,11 @@ struct GroupedGemm {
     // [0, a_rows)) instead of row p -- the dispatch gather folded into the loads.
     const int32_t* gather;
     int64_t a_rows;
+    // Down-projection, top-1 only: grouped row p is stored as w[t] * row into row
+    // t = scatter[p] (clamped to [0, c_rows)) of c instead of row p -- Step 5 folded in.
+    const int32_t* scatter;
+    const float* scatter_w;
+    int64_t c_rows;
 };
 
 // Source row of grouped row p: p itself, or gather[p] clamped into a (entries past the
@@ -616,8 +621,15 @@ void gemm_bf16_lds(GroupedGemm g) {
         const int64_t row_lo = t.row0 > 0 ? t.row0 : 0;
 #pragma unroll
         for (int i = 0; i < MI; ++i) {
-            const int64_t row = t.row_base + wm * (BM / 2) + i * 32 + l32;
+            int64_t row = t.row_base + wm * (BM / 2) + i * 32 + l32;
             const bool row_ok = row >= row_lo && row < t.row_end;
+            float scale = 1.f;
+            if (!kUp && g.scatter) {
+                // the grouped row's token and gate weight (one index load per tile and row)
+                const int64_t src = row_ok ? g.scatter[row] : 0;
+                row = src < 0 ? 0 : (src >= g.c_rows ? g.c_rows - 1 : src);
+                scale = row_ok ? g.scatter_w[row] : 0.f;
+            }
 #pragma unroll
             for (int j = 0; j < NI; ++j)
 #pragma unroll
@@ -626,8 +638,8 @@ void gemm_bf16_lds(GroupedGemm g) {
                     float v[4];
 #pragma unroll
                     for (int c = 0; c < 4; ++c)
-                        v[c] = epilogue_fast<EPI>(acc_read<kAccInAgpr>(acc[0][i][j][4 * q + c]),
-                                                  acc_read<kAccInAgpr>(acc[NB - 1][i][j][4 * q + c]));
+                        v[c] = scale * epilogue_fast<EPI>(acc_read<kAccInAgpr>(acc[0][i][j][4 * q + c]),
+                                                          acc_read<kAccInAgpr>(acc[NB - 1][i][j][4 * q + c]));
                     if (row_ok && col >= t.n0 && col < g.N) {
                         // 4 columns col .. col + 3 never cross a 32-column block
                         const int64_t ci = kUp ? ((static_cast<int64_t>(col) >> 5) * g.rows_max + row) * 32 + (col & 31)
@@ -717,11 +729,17 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GroupedGemm g) {
     if (n >= g.N) return;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int64_t row = row0 + ty * 4 + i;
+        int64_t row = row0 + ty * 4 + i;
         if (row >= row_end) break;
+        float scale = 1.f;
+        if (g.scatter) {
+            const int64_t src = g.scatter[row];
+            row = src < 0 ? 0 : (src >= g.c_rows ? g.c_rows - 1 : src);
+            scale = g.scatter_w[row];
+        }
         float v[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = epilogue<EPI>(acc[0][i][j], acc[NB - 1][i][j]);
+        for (int j = 0; j < 4; ++j) v[j] = scale * epilogue<EPI>(acc[0][i][j], acc[NB - 1][i][j]);
         if (OB) {
             uint2 q;
             q.x = pack_bf16x2(v[0], v[1]);
@@ -825,7 +843,7 @@ hipError_t gemm1(bool bf16, GroupedGemm g, int64_t A_max, hipStream_t s) {
 hipError_t ffn_pair(const void* x_perm, const int32_t* offsets, int64_t grid_rows, int64_t rows_max, int E,
                     int h, int64_t fp, int act, bool bf16, const void* w1t, const void* w3t, const void* w2t,
                     void* y_perm, bool y_bf16, void* hbuf, hipStream_t s, const int32_t* gather = nullptr,
-                    int64_t a_rows = 0) {
+                    int64_t a_rows = 0, const float* scatter_w = nullptr) {
     if (grid_rows == 0) return hipSuccess;
     GroupedGemm g1{};
     g1.a = x_perm;
@@ -859,6 +877,11 @@ hipError_t ffn_pair(const void* x_perm, const int32_t* offsets, int64_t grid_row
     g2.ldc = h;
     g2.b_estride = static_cast<int64_t>(h) * fp;
     g2.rows_max = rows_max;
+    if (scatter_w) {
+        g2.scatter = gather;
+        g2.scatter_w = scatter_w;
+        g2.c_rows = a_rows;
+    }
     if (bf16)
         return y_bf16 ? run_bf16_best<kEpiNone, true>(g2, grid_rows, s) : run_bf16_best<kEpiNone, false>(g2, grid_rows, s);
     return y_bf16 ? run_f32<kEpiNone, true>(g2, grid_rows, s) : run_f32<kEpiNone, false>(g2, grid_rows, s);
@@ -881,6 +904,15 @@ hipError_t launch_ffn_gather(const void* x, int64_t T, const int32_t* row_src, c
 // One expert at a time: expert e's segment is the one-expert grouping (offsets + e), its
 // weights start e matrices into each packed block, and the launches are sized by its own
 // row count, read from the host copy of the offsets.
+// Top-1 layer output in one call: gathered rows in, y[t] = w[t] * FFN(x[t]) out.
+hipError_t launch_ffn_top1(const void* x, int64_t T, const int32_t* row_src, const float* topk_w,
+                           const int32_t* offsets, int64_t A_max, int E, int h, int64_t fp, int act, bool bf16,
+                           const void* w1t, const void* w3t, const void* w2t, void* y, bool y_bf16, void* hbuf,
+                           hipStream_t s) {
+    return ffn_pair(x, offsets, A_max, A_max, E, h, fp, act, bf16, w1t, w3t, w2t, y, y_bf16, hbuf, s, row_src, T,
+                    topk_w);
+}
+
 hipError_t launch_ffn_per_expert(const void* x_perm, const int32_t* offsets, const int32_t* offsets_host,
                                  int64_t A_max, int E, int h, int64_t fp, int act, bool bf16, const void* w1t,
                                  const void* w3t, const void* w2t, void* y_perm, bool y_bf16, void* hbuf,

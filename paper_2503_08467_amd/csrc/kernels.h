@@ -31,6 +31,11 @@ hipError_t launch_ffn_gather(const void* x, int64_t T, const int32_t* row_src, c
                              int E, int h, int64_t fp, int act, bool bf16, const void* w1t, const void* w3t,
                              const void* w2t, void* y_perm, bool y_bf16, void* hbuf, hipStream_t s);
 
+hipError_t launch_ffn_top1(const void* x, int64_t T, const int32_t* row_src, const float* topk_w,
+                           const int32_t* offsets, int64_t A_max, int E, int h, int64_t fp, int act, bool bf16,
+                           const void* w1t, const void* w3t, const void* w2t, void* y, bool y_bf16, void* hbuf,
+                           hipStream_t s);
+
 hipError_t launch_ffn_per_expert(const void* x_perm, const int32_t* offsets, const int32_t* offsets_host,
                                  int64_t A_max, int E, int h, int64_t fp, int act, bool bf16, const void* w1t,
                                  const void* w3t, const void* w2t, void* y_perm, bool y_bf16, void* hbuf,

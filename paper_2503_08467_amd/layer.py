@@ -202,6 +202,30 @@ def expert_ffn_shard_gather(x: torch.Tensor, row_src: torch.Tensor, offsets: tor
     return out
 
 
+def expert_ffn_shard_top1(x: torch.Tensor, row_src: torch.Tensor, topk_w: torch.Tensor, offsets: torch.Tensor,
+                          packed: PackedShard, out_dtype: Optional[torch.dtype] = None,
+                          out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                          stream=None) -> torch.Tensor:
+    """Steps 4 and 5 for top-1 routing: y[t] = topk_w[t] * FFN_shard(x[t]) in one call."""
+    _dev(x, "x"), _dev(row_src, "row_src"), _dev(topk_w, "topk_w"), _dev(offsets, "offsets")
+    if x.dtype != packed.dtype:
+        raise TypeError("x must have the packed weights' dtype")
+    if row_src.dtype != torch.int32 or topk_w.dtype != torch.float32:
+        raise TypeError("row_src must be int32 and topk_w float32")
+    T = x.shape[0]
+    if row_src.numel() != T or topk_w.numel() != T:
+        raise ValueError("top-1: row_src and topk_w must have one entry per token")
+    out_dtype = out_dtype or x.dtype
+    if out is None:
+        out = torch.empty((T, packed.h), dtype=out_dtype, device=x.device)
+    if ws is None:
+        ws = torch.empty(max(ffn_workspace_size(T, packed), 16), dtype=torch.uint8, device=x.device)
+    _lib.call("moe_expert_ffn_shard_top1", _ptr(x), T, _ptr(row_src), _ptr(topk_w), _ptr(offsets), packed.E,
+              packed.h, packed.f, _lib.ACTS[packed.act], _DT[packed.dtype], _ptr(packed.buf), _ptr(out), _dt(out),
+              _ptr(ws), ws.numel(), _stream(x, stream))
+    return out
+
+
 def expert_ffn_shard_per_expert(x_perm: torch.Tensor, offsets: torch.Tensor, packed: PackedShard,
                                 out_dtype: Optional[torch.dtype] = None, A_max: Optional[int] = None,
                                 out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
@@ -290,13 +314,18 @@ class MoEShardLayer:
         d = Dispatch(self.disp.counts, self.disp.offsets, self.disp.row_src[:T * k], self.disp.pos_of[:T],
                      None if self.disp.x_perm is None else self.disp.x_perm[:T * k])
         dispatch(idx, x, self.E, out=d, ws=self.dws)
-        if d.x_perm is None:
-            y_perm = expert_ffn_shard_gather(x, d.row_src, d.offsets, self.packed, A_max=T * k,
-                                             out=self.y_perm[:T * k], ws=self.fws)
+        if d.x_perm is None and k == 1:
+            # top-1: the expert step writes the weighted rows straight into y
+            y_perm = None
+            y = expert_ffn_shard_top1(x, d.row_src, w.view(-1), d.offsets, self.packed, out=self.y[:T], ws=self.fws)
         else:
-            y_perm = expert_ffn_shard(d.x_perm, d.offsets, self.packed, A_max=T * k, out=self.y_perm[:T * k],
-                                      ws=self.fws)
-        y = combine(y_perm, d.pos_of, w, out=self.y[:T])
+            if d.x_perm is None:
+                y_perm = expert_ffn_shard_gather(x, d.row_src, d.offsets, self.packed, A_max=T * k,
+                                                 out=self.y_perm[:T * k], ws=self.fws)
+            else:
+                y_perm = expert_ffn_shard(d.x_perm, d.offsets, self.packed, A_max=T * k, out=self.y_perm[:T * k],
+                                          ws=self.fws)
+            y = combine(y_perm, d.pos_of, w, out=self.y[:T])
         self.last = dict(idx=idx, w=w, dispatch=d, y_perm=y_perm)
         return y
 

@@ -251,6 +251,41 @@ def test_gathered_rows_match_x_perm(dtype, act, T, k, E, h, f):
     assert rowwise(np_of(y_gath[:n]), ref) <= TOL[dtype]
 
 
+@pytest.mark.parametrize("dtype,out_dtype", [("bf16", "bf16"), ("bf16", "f32"), ("f32", "f32")])
+@pytest.mark.parametrize("act", ["gelu", "swiglu"])
+@pytest.mark.parametrize("T,E,h,f", [(700, 6, 256, 200), (90, 3, 72, 128), (1300, 5, 768, 384)])
+def test_top1_step_writes_weighted_rows(dtype, out_dtype, act, T, E, h, f):
+    """moe_expert_ffn_shard_top1 = the expert step plus the top-1 combine: y[t] = w[t] *
+    FFN_e(x[t]).  Tokens whose only pick is invalid are dropped and left unwritten."""
+    rng = np.random.default_rng(T + E + h)
+    x = rng.standard_normal((T, h)).astype(np.float32)
+    w1 = (rng.standard_normal((E, h, f)) * 0.05).astype(np.float32)
+    w3 = (rng.standard_normal((E, h, f)) * 0.05).astype(np.float32) if act == "swiglu" else None
+    w2 = (rng.standard_normal((E, f, h)) * 0.05).astype(np.float32)
+    if dtype == "bf16":
+        x, w1, w2 = synth.round_to_bf16(x), synth.round_to_bf16(w1), synth.round_to_bf16(w2)
+        w3 = None if w3 is None else synth.round_to_bf16(w3)
+    idx = rng.integers(0, E + 1, size=(T, 1)).astype(np.int32)  # id E is invalid: dropped
+    wt = rng.uniform(0.1, 1.0, size=(T, 1)).astype(np.float32)
+    dt, odt = tdt(dtype), tdt(out_dtype)
+    xd = to_dev(x, dt)
+    packed = moe.pack_weights(to_dev(w1, dt), to_dev(w2, dt), to_dev(w3, dt), f=f, act=act)
+    d = moe.dispatch(to_dev(idx, torch.int32), xd, E, x_perm=False)
+    y = torch.full((T, h), 7.0, dtype=odt, device="cuda")
+    moe.expert_ffn_shard_top1(xd, d.row_src, to_dev(wt, torch.float32).view(-1), d.offsets, packed, out=y)
+    torch.cuda.synchronize()
+    y = np_of(y)
+    valid = idx[:, 0] < E
+    assert (~valid).any() and valid.any()
+    offsets = d.offsets.cpu().numpy()
+    row_src = d.row_src.cpu().numpy()[:offsets[-1]]
+    y_perm = oracle.expert_ffn(x[row_src], offsets, w1, w3, w2, act)
+    ref = np.zeros((T, h))
+    ref[row_src] = y_perm * wt[row_src]
+    assert rowwise(y[valid], ref[valid]) <= TOL[out_dtype if dtype == "bf16" and out_dtype == "bf16" else dtype]
+    assert np.all(y[~valid] == 7.0)
+
+
 @pytest.mark.parametrize("g", [0, 1, 2, 3])
 def test_ffn_shard_slice_of_full_weights(g):
     """moe_pack_weights cuts shard g (inner columns [g*f, (g+1)*f)) out of the full weights;
@@ -340,7 +375,8 @@ def test_layer_end_to_end(name, T, fused):
         assert np.array_equal(by_expert(d.pos_of.cpu().numpy(), gi), by_expert(ref["pos_of"], ref["idx"]))
         if d.x_perm is not None:
             assert np.array_equal(np_of(d.x_perm), ref["x_perm"])
-        assert rowwise(np_of(last["y_perm"]), ref["y_perm"]) <= tol
+        if last["y_perm"] is not None:  # top-1 with the fused gather writes y directly
+            assert rowwise(np_of(last["y_perm"]), ref["y_perm"]) <= tol
     else:
         print(f"{name}: {(~same_set).sum()} tokens picked a different but equally valid set")
     assert rowwise(np_of(y)[same_set], ref["y"][same_set]) <= tol
