@@ -24,6 +24,7 @@
 
 #include <algorithm>
 #include <mutex>
+#include <type_traits>
 
 namespace moe {
 namespace {
@@ -537,18 +538,21 @@ void gemm_bf16_lds(GroupedGemm g) {
     for (int st = 0; st < NS - 1; ++st) issue_next();
 
     // ---- fragments: A block i = activation rows wm*BM/2 + 32 i + l32, B block (nb, j) =
-    // weight rows BM + nb*BN + wn*BN/2 + 32 j + l32; K chunk 2 ks + lhi of the stage
+    // weight rows BM + nb*BN + wn*BN/2 + 32 j + l32; K chunk 2 ks + lhi of the stage.  Only
+    // the first NV row blocks of the wave are read (the rest hold no valid row).
     const int wm = wave >> 1, wn = wave & 1;
     const int l32 = lane & 31, lhi = lane >> 5;
     typedef bf16x8_t Frags[MI + NB * NI];
-    auto read_frags = [&](int stage_slot, int ks, Frags& f) {
+    auto read_frags = [&](auto nv_tag, int stage_slot, int ks, Frags& f) {
+        constexpr int NV = decltype(nv_tag)::value;
         const unsigned char* st = smem_raw + stage_slot * kStageBytes;
         const int ch = 2 * ks + lhi;
 #pragma unroll
-        for (int i = 0; i < MI; ++i) {
+        for (int i = 0; i < NV; ++i) {
             const int R = wm * (BM / 2) + i * 32 + l32;
             f[i] = *reinterpret_cast<const bf16x8_t*>(st + R * (2 * BK) + ((ch ^ ((R >> SH) & (CPR - 1))) << 4));
         }
+        if (NV == 0) return;
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
@@ -563,6 +567,17 @@ void gemm_bf16_lds(GroupedGemm g) {
     constexpr bool kAccInAgpr = S::kPerCU == 1;
     int consumed = 0;
     for (int ct = t_first; ct < t_end; ct += nslot) {
+        const TileGeom t = tile_geom<BM, BN>(g, tstart, total_m, ct);
+        // Row blocks of this wave that hold valid rows.  Valid rows start at the tile's first
+        // row unless the tile was shifted back at the end of the buffer; then all count.  The
+        // count is rounded up to MI / 2 or MI so that three loop bodies cover every case.
+        int nv = MI;
+        if (t.row_base == t.row0) {
+            const int64_t left = t.row_end - (t.row0 + wm * (BM / 2));
+            nv = left <= 0 ? 0 : (left > (MI / 2) * 32 ? MI : MI / 2);
+        }
+        nv = __builtin_amdgcn_readfirstlane(nv);
+
         f32x16_t acc[NB][MI][NI];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
@@ -572,55 +587,66 @@ void gemm_bf16_lds(GroupedGemm g) {
                 for (int j = 0; j < NI; ++j)
 #pragma unroll
                     for (int r = 0; r < 16; ++r) acc[nb][i][j][r] = 0.f;
-        auto mma = [&](const Frags& f) {
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                for (int i = 0; i < MI; ++i)
-#pragma unroll
-                    for (int j = 0; j < NI; ++j)
-                        acc[nb][i][j] =
-                            __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[MI + nb * NI + j], f[i], acc[nb][i][j], 0, 0, 0);
-        };
 
         // publish the tile's first stage; after an epilogue its stores share the counter
         if (ct != t_first) wait_vmcnt<0>();
         else wait_stages<LPW, NS>(issued - consumed - 1);
         stage_barrier();
         issue_next();
-        Frags f0, f1;
-        read_frags(consumed % NS, 0, f0);
 
-        for (int ck = 0; ck < nk; ++ck) {
-            const int slot = consumed % NS;
+        // the K loop with the MFMAs of the first NV row blocks; every wave takes part in the
+        // loads, waits and barriers whatever its NV
+        auto k_loop = [&](auto nv_tag) {
+            constexpr int NV = decltype(nv_tag)::value;
+            // weight block outer, row block inner: consecutive MFMAs share their first operand
+            auto mma = [&](const Frags& f) {
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                Frags& cur = (ks & 1) ? f1 : f0;
-                Frags& nxt = (ks & 1) ? f0 : f1;
-                if (ks + 1 < KS) {
-                    read_frags(slot, ks + 1, nxt);
-                } else if (ck + 1 < nk) {
-                    // publish stage consumed + 1 (see above), refill, start its fragments
-                    wait_lgkm0();
-                    wait_stages<LPW, NS>(issued - consumed - 2);
-                    stage_barrier();
-                    issue_next();
-                    read_frags((consumed + 1) % NS, 0, nxt);
+                for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                    for (int j = 0; j < NI; ++j)
+#pragma unroll
+                        for (int i = 0; i < NV; ++i)
+                            acc[nb][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[MI + nb * NI + j], f[i],
+                                                                                    acc[nb][i][j], 0, 0, 0);
+            };
+            Frags f0, f1;
+            read_frags(nv_tag, consumed % NS, 0, f0);
+            for (int ck = 0; ck < nk; ++ck) {
+                const int slot = consumed % NS;
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    Frags& cur = (ks & 1) ? f1 : f0;
+                    Frags& nxt = (ks & 1) ? f0 : f1;
+                    if (ks + 1 < KS) {
+                        read_frags(nv_tag, slot, ks + 1, nxt);
+                    } else if (ck + 1 < nk) {
+                        // publish stage consumed + 1 (see above), refill, start its fragments
+                        wait_lgkm0();
+                        wait_stages<LPW, NS>(issued - consumed - 2);
+                        stage_barrier();
+                        issue_next();
+                        read_frags(nv_tag, (consumed + 1) % NS, 0, nxt);
+                    }
+                    if (NV > 0) {
+                        mma(cur);
+                        interleave_reads<NB * NV * NI, NV + NB * NI>();
+                    }
                 }
-                mma(cur);
-                interleave_reads<NB * MI * NI, MI + NB * NI>();
+                // KS is even for BK 32 / 64, so the next step's first fragments are in f0
+                ++consumed;
             }
-            // KS is even for BK 32 / 64, so the next step's first fragments are in f0
-            ++consumed;
-        }
+        };
+        if (nv == MI) k_loop(std::integral_constant<int, MI>());
+        else if (nv > 0) k_loop(std::integral_constant<int, MI / 2>());
+        else k_loop(std::integral_constant<int, 0>());
 
         // ---- epilogue of tile ct.  D[n][m] layout: lane holds activation row l32 of the
         // block; register r holds weight row 8 * (r / 4) + 4 * lhi + r % 4, i.e. 4
         // consecutive output columns per group r / 4.
-        const TileGeom t = tile_geom<BM, BN>(g, tstart, total_m, ct);
         const int64_t row_lo = t.row0 > 0 ? t.row0 : 0;
 #pragma unroll
         for (int i = 0; i < MI; ++i) {
+            if (i >= nv) break;  // no valid row in this block or any later one
             int64_t row = t.row_base + wm * (BM / 2) + i * 32 + l32;
             const bool row_ok = row >= row_lo && row < t.row_end;
             float scale = 1.f;
