@@ -58,16 +58,16 @@ __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 //     t = 1 / (1 + p a),  |eps| <= 1.5e-7.
 // GELU(u) = u Phi(u) = u (1 + erf(u / sqrt 2)) / 2; with Q = (poly) exp(-a^2), a = |u|/sqrt 2:
 //     u >= 0:  u (1 - Q / 2)        u < 0:  u Q / 2
+// The constants are folded for the vector unit: t = 1 / (1 + (p / sqrt 2) |u|), the
+// coefficients carry the 1/2, and exp(-a^2) = 2^(-u^2 log2(e) / 2).
 __device__ __forceinline__ float act_gelu_fast(float u) {
-    const float a = fabsf(u) * 0.70710678118654752f;
-    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, a, 1.0f));
-    float poly = 1.061405429f;
-    poly = fmaf(poly, t, -1.453152027f);
-    poly = fmaf(poly, t, 1.421413741f);
-    poly = fmaf(poly, t, -0.284496736f);
-    poly = fmaf(poly, t, 0.254829592f);
-    poly *= t;
-    const float q = 0.5f * poly * __expf(-a * a);
+    const float t = __builtin_amdgcn_rcpf(fmaf(fabsf(u), 0.3275911f * 0.70710678118654752f, 1.0f));
+    float poly = 0.5f * 1.061405429f;
+    poly = fmaf(poly, t, 0.5f * -1.453152027f);
+    poly = fmaf(poly, t, 0.5f * 1.421413741f);
+    poly = fmaf(poly, t, 0.5f * -0.284496736f);
+    poly = fmaf(poly, t, 0.5f * 0.254829592f);
+    const float q = poly * t * __builtin_amdgcn_exp2f((u * -0.72134752044448170f) * u);
     return u >= 0.f ? u - u * q : u * q;
 }
 

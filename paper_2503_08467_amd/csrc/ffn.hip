@@ -642,7 +642,9 @@ void gemm_bf16_lds(GroupedGemm g) {
 
         // ---- epilogue of tile ct.  D[n][m] layout: lane holds activation row l32 of the
         // block; register r holds weight row 8 * (r / 4) + 4 * lhi + r % 4, i.e. 4
-        // consecutive output columns per group r / 4.
+        // consecutive output columns per group r / 4.  The lane's address is formed once per
+        // 32-column block; its four groups sit 8 elements apart (immediate store offsets).
+        typedef typename std::conditional<OB, bf16_t, float>::type OutT;
         const int64_t row_lo = t.row0 > 0 ? t.row0 : 0;
 #pragma unroll
         for (int i = 0; i < MI; ++i) {
@@ -657,32 +659,36 @@ void gemm_bf16_lds(GroupedGemm g) {
                 scale = row_ok ? g.scatter_w[row] : 0.f;
             }
 #pragma unroll
-            for (int j = 0; j < NI; ++j)
+            for (int j = 0; j < NI; ++j) {
+                // this lane's first column in the block; the 4-column groups col .. col + 3
+                // never cross a 32-column block (K-blocked H) nor the end of a row (N % 4 == 0)
+                const int col0 = t.n_base + wn * (BN / 2) + j * 32 + 4 * lhi;
+                OutT* const dst = static_cast<OutT*>(g.c) +
+                                  (kUp ? ((static_cast<int64_t>(col0) >> 5) * g.rows_max + row) * 32 + (col0 & 31)
+                                       : row * g.ldc + col0);
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int col = t.n_base + wn * (BN / 2) + j * 32 + 8 * q + 4 * lhi;
+                    const int col = col0 + 8 * q;
                     float v[4];
 #pragma unroll
                     for (int c = 0; c < 4; ++c)
                         v[c] = scale * epilogue_fast<EPI>(acc_read<kAccInAgpr>(acc[0][i][j][4 * q + c]),
                                                           acc_read<kAccInAgpr>(acc[NB - 1][i][j][4 * q + c]));
                     if (row_ok && col >= t.n0 && col < g.N) {
-                        // 4 columns col .. col + 3 never cross a 32-column block
-                        const int64_t ci = kUp ? ((static_cast<int64_t>(col) >> 5) * g.rows_max + row) * 32 + (col & 31)
-                                               : row * g.ldc + col;
                         if (OB) {
                             uint2 pk;
                             pk.x = pack_bf16x2(v[0], v[1]);
                             pk.y = pack_bf16x2(v[2], v[3]);
-                            *reinterpret_cast<uint2*>(static_cast<bf16_t*>(g.c) + ci) = pk;
+                            *reinterpret_cast<uint2*>(dst + 8 * q) = pk;
                         } else {
-                            *reinterpret_cast<float4*>(static_cast<float*>(g.c) + ci) = make_float4(v[0], v[1], v[2], v[3]);
+                            *reinterpret_cast<float4*>(dst + 8 * q) = make_float4(v[0], v[1], v[2], v[3]);
                         }
                     }
-                    // one block at a time: keeps the scheduler from pulling every accumulator
+                    // one group at a time: keeps the scheduler from pulling every accumulator
                     // into VGPRs at once
                     __builtin_amdgcn_sched_barrier(0);
                 }
+            }
         }
     }
 }
