@@ -10,7 +10,11 @@
 //           assignment's position is   chunk base + earlier waves' count + running count
 //           + number of lower lanes with the same expert   -- stable in (t, j) order
 //   gather  x_perm[p] = x[row_src[p]] with 16-byte vector copies
-// Integer atomics are used only for the LDS histogram, whose result does not depend on
+// Up to kFusedMaxA assignments, count, scan and rank run as one kernel instead (same
+// output): every chunk's workgroup counts all assignments itself into per-wave LDS
+// histograms, keeping the counts of the chunks before its own apart, scans the totals,
+// and ranks its chunk as above.  Three dependent launches of a few microseconds each become one.
+// Integer atomics are used only for the LDS histograms, whose result does not depend on
 // their order.
 #include "common.h"
 #include "kernels.h"
@@ -134,6 +138,138 @@ __global__ __launch_bounds__(kDispThreads) void dispatch_rank(const int32_t* __r
     }
 }
 
+constexpr int64_t kFusedMaxA = 16384;
+constexpr int kFusedBatch = 16;  // groups of 64 assignments whose loads are issued together
+
+// Lanes of this wave whose expert equals this lane's (valid lanes only), from nbits ballots.
+__device__ __forceinline__ uint64_t same_expert_lanes(int e, bool valid, int nbits) {
+    uint64_t peers = __ballot(valid);
+    for (int b = 0; b < nbits; ++b) {
+        const bool bit = valid && ((e >> b) & 1);
+        const uint64_t m = __ballot(bit);
+        peers &= bit ? m : ~m;
+    }
+    return peers;
+}
+
+__global__ __launch_bounds__(kDispThreads) void dispatch_fused(const int32_t* __restrict__ idx, int64_t A, int k,
+                                                               int E, int nbits, int32_t* __restrict__ counts,
+                                                               int32_t* __restrict__ offsets,
+                                                               int32_t* __restrict__ row_src,
+                                                               int32_t* __restrict__ pos_of) {
+    __shared__ int tot[MOE_MAX_EXPERTS];
+    __shared__ int before[MOE_MAX_EXPERTS];
+    __shared__ int off[MOE_MAX_EXPERTS + 1];
+    __shared__ int wcnt[kDispWaves][MOE_MAX_EXPERTS];
+    __shared__ int run[kDispWaves][MOE_MAX_EXPERTS];
+    __shared__ int wtot[kDispWaves][MOE_MAX_EXPERTS];
+    __shared__ int wbef[kDispWaves][MOE_MAX_EXPERTS];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int c = blockIdx.x;
+    const int64_t cbeg = static_cast<int64_t>(c) * kDispatchChunk;
+    for (int e = lane; e < E; e += kWave) wcnt[wave][e] = wtot[wave][e] = wbef[wave][e] = 0;
+    __syncthreads();
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+
+    // every assignment, 64 at a time per wave (kFusedBatch groups' loads in flight together),
+    // into this wave's histograms
+    for (int64_t b0 = static_cast<int64_t>(wave) * kWave; b0 < A; b0 += kDispThreads * kFusedBatch) {
+        int eb[kFusedBatch];
+#pragma unroll
+        for (int u = 0; u < kFusedBatch; ++u) {
+            const int64_t a = b0 + static_cast<int64_t>(u) * kDispThreads + lane;
+            eb[u] = (a < A) ? idx[a] : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < kFusedBatch; ++u) {
+            const int64_t a = b0 + static_cast<int64_t>(u) * kDispThreads + lane;
+            const int e = eb[u];
+            if (static_cast<unsigned>(e) < static_cast<unsigned>(E)) {
+                atomicAdd(&wtot[wave][e], 1);
+                if (a < cbeg) atomicAdd(&wbef[wave][e], 1);
+            }
+        }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < E; e += kDispThreads) {
+        int t = 0, b = 0;
+#pragma unroll
+        for (int w = 0; w < kDispWaves; ++w) {
+            t += wtot[w][e];
+            b += wbef[w][e];
+        }
+        tot[e] = t;
+        before[e] = b;
+    }
+    __syncthreads();
+
+    // exclusive scan of the totals: one wave, four experts per lane
+    if (wave == 0) {
+        int ex[4], sum = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int e = lane * 4 + i;
+            ex[i] = sum;
+            sum += (e < E) ? tot[e] : 0;
+        }
+        int incl = sum;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const int t = __shfl_up(incl, o, kWave);
+            if (lane >= o) incl += t;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int e = lane * 4 + i;
+            if (e < E) off[e] = incl - sum + ex[i];
+        }
+        if (lane == kWave - 1) off[E] = incl;
+    }
+    __syncthreads();
+    if (c == 0) {
+        for (int e = threadIdx.x; e <= E; e += kDispThreads) {
+            offsets[e] = off[e];
+            if (e < E) counts[e] = tot[e];
+        }
+    }
+
+    // rank this chunk's assignments (as in dispatch_rank, with base = off + before)
+    const int64_t a0 = cbeg + wave * kPerWave;
+    int ev[kRounds];
+#pragma unroll
+    for (int s = 0; s < kRounds; ++s) {
+        const int64_t a = a0 + s * kWave + lane;
+        ev[s] = (a < A) ? idx[a] : -1;
+        if (static_cast<unsigned>(ev[s]) < static_cast<unsigned>(E)) atomicAdd(&wcnt[wave][ev[s]], 1);
+    }
+    __syncthreads();
+    for (int e = lane; e < E; e += kWave) {
+        int b = off[e] + before[e];
+        for (int w = 0; w < wave; ++w) b += wcnt[w][e];
+        run[wave][e] = b;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int s = 0; s < kRounds; ++s) {
+        const int64_t a = a0 + s * kWave + lane;
+        const int e = ev[s];
+        const bool valid = static_cast<unsigned>(e) < static_cast<unsigned>(E);
+        const uint64_t peers = same_expert_lanes(e, valid, nbits);
+        const int rank = __popcll(peers & lt);
+        if (valid) {
+            const int pos = run[wave][e] + rank;
+            pos_of[a] = pos;
+            if (pos >= 0 && pos < A) row_src[pos] = static_cast<int32_t>(a / k);
+        } else if (a < A) {
+            pos_of[a] = -1;
+        }
+        __syncthreads();  // every lane has read run[] before the group leaders advance it
+        if (valid && rank == 0) run[wave][e] += __popcll(peers);
+        __syncthreads();
+    }
+}
+
 // x_perm[p] = x[row_src[p]] for p < offsets[E]: each wave copies kGatherRows rows, its lanes
 // striding over the 16-byte vectors of a row, with the loads of all its rows issued before
 // their stores.
@@ -176,14 +312,21 @@ hipError_t launch_dispatch(const int32_t* idx, int64_t T, int k, int E, const vo
     int32_t* base = ws + static_cast<int64_t>(E) * nchunks;
     int nbits = 0;
     while ((1 << nbits) < E) ++nbits;
-    if (nchunks > 0) {
-        hipLaunchKernelGGL(dispatch_count, dim3(nchunks), dim3(kDispThreads), 0, s, idx, A, E, nchunks, cc);
+    if (nchunks > 0 && A <= kFusedMaxA) {
+        hipLaunchKernelGGL(dispatch_fused, dim3(nchunks), dim3(kDispThreads), 0, s, idx, A, k, E, nbits, counts,
+                           offsets, row_src, pos_of);
+    } else {
+        if (nchunks > 0) {
+            hipLaunchKernelGGL(dispatch_count, dim3(nchunks), dim3(kDispThreads), 0, s, idx, A, E, nchunks, cc);
+        }
+        hipLaunchKernelGGL(dispatch_scan, dim3(1), dim3(kScanThreads), 0, s, cc, E, nchunks, base, counts,
+                           offsets);
+        if (nchunks > 0) {
+            hipLaunchKernelGGL(dispatch_rank, dim3(nchunks), dim3(kDispThreads), 0, s, idx, A, k, E, nbits,
+                               nchunks, base, row_src, pos_of);
+        }
     }
-    hipLaunchKernelGGL(dispatch_scan, dim3(1), dim3(kScanThreads), 0, s, cc, E, nchunks, base, counts,
-                       offsets);
     if (nchunks > 0) {
-        hipLaunchKernelGGL(dispatch_rank, dim3(nchunks), dim3(kDispThreads), 0, s, idx, A, k, E, nbits,
-                           nchunks, base, row_src, pos_of);
         if (x_perm) {  // without x_perm the expert step gathers the rows itself
             const uint32_t nvec = static_cast<uint32_t>(static_cast<int64_t>(h) * elem_bytes / 16);
             const int64_t blocks = ceil_div(A, 4 * kGatherRows);
