@@ -121,8 +121,11 @@ def _check_dispatch(idx, E, h=64, dtype=torch.bfloat16):
     assert torch.equal(d.x_perm[:A], xd[src])
 
 
+# up to 16384 assignments one fused kernel dispatches, above it three kernels: both sides of
+# that boundary are covered (8192 x 2, 16384 x 1 fused; 16385 x 1 and larger not)
 @pytest.mark.parametrize("T,k,E", [(0, 1, 8), (1, 1, 1), (5, 2, 5), (1000, 1, 64), (1023, 2, 7), (1024, 2, 256),
-                                   (3000, 3, 100), (16384, 1, 128), (32768, 2, 64), (4096, 8, 256)])
+                                   (3000, 3, 100), (8192, 2, 3), (16384, 1, 128), (16385, 1, 64), (32768, 2, 64),
+                                   (4096, 8, 256)])
 def test_dispatch_bit_exact(T, k, E):
     rng = np.random.default_rng(T + 7 * E)
     p = rng.dirichlet(np.full(E, 0.3))  # skewed popularity, many empty experts
