@@ -854,15 +854,24 @@ hipError_t run_bf16_lds(GroupedGemm g, int64_t A_max, hipStream_t s) {
 // The up-projection needs h % 32 == 0 for the pipelined kernel (the packed W1 is K-blocked
 // exactly then); otherwise the register-staged kernel runs it on row-major weights and still
 // writes H K-blocked.  The down-projection's K is fp, always a multiple of 128.
+//
+// When the down-projection's tiles fit on the CUs in one round even 384 columns wide (few
+// rows, e.g. a top-1 layer of a few thousand tokens or a decode batch), it runs 128 x 384
+// tiles, one workgroup per CU with 96 KiB of stages: every tile then streams its weights
+// with more bytes in flight instead of a third of the CUs taking a second tile.  Each
+// output element's K sum is the same in either shape.
 template <int EPI, bool OB>
 hipError_t run_bf16_best(GroupedGemm g, int64_t A_max, hipStream_t s) {
     constexpr bool kUp = EPI != kEpiNone;
-    if (kUp) {
+    if constexpr (kUp) {
         if (g.K % 32 == 0) return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);
         return run_bf16<EPI, OB, true>(g, A_max, s);
+    } else {
+        if (g.K % 32 != 0) return hipErrorInvalidValue;  // not reachable through the C ABI (fp % 128 == 0)
+        if (g.N >= 384 && row_tile_bound(A_max, g.E, 128) * ceil_div(g.N, 384) <= device_cus())
+            return run_bf16_lds<128, 384, 32, 3, EPI, OB>(g, A_max, s);
+        return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);
     }
-    if (g.K % 32 == 0) return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);  // down-projection
-    return hipErrorInvalidValue;  // not reachable through the C ABI (fp % 128 == 0)
 }
 
 template <int EPI>
