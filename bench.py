@@ -3,7 +3,7 @@
 One step = one full layer forward (route -> dispatch -> expert FFN shard -> combine) over
 one batch of synthetic tokens already resident in HBM.  Prints one JSON line.
 
-  python bench.py [--steps K] [--warmup W] [--config c2] [--no-cpu-baseline]
+  python bench.py [--steps K] [--warmup W] [--config c2] [--no-cpu-baseline] [--cold-steps N]
   python bench.py --ablation        # grouped vs per-expert launches, E = 8 .. 256
 
 HBM traffic of the expert-FFN kernels comes from two rocprofv3 counter runs of this script,
@@ -194,6 +194,8 @@ def main():
     ap.add_argument("--config", default="c2")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cold-steps", type=int, default=0,
+                    help="after the timed steps, this many more, each after a 512 MiB cache flush (cold_cache)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run an untimed plain copy of this size first (counter calibration)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
@@ -268,13 +270,41 @@ def main():
     for _ in range(args.warmup):
         step()
     ffn_events = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    step_events = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
+        step_events[i].record(stream)
         step(ffn_ev=ffn_events[i])
+    step_events[-1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ffn_us = float(np.mean([a.elapsed_time(b) for a, b in ffn_events])) * 1e3
+    ffn_each = np.array([a.elapsed_time(b) for a, b in ffn_events]) * 1e3
+    ffn_us = float(np.mean(ffn_each))
+    step_each = np.array([step_events[i].elapsed_time(step_events[i + 1]) for i in range(args.steps)]) * 1e3
+
+    def spread(v):
+        return {"median": round(float(np.median(v)), 2), "p10": round(float(np.percentile(v, 10)), 2),
+                "p90": round(float(np.percentile(v, 90)), 2)}
+
+    # cold caches: a separate pass that overwrites 512 MiB (more than L2 and MALL together)
+    # before every step, outside the events
+    cold = None
+    if args.cold_steps:
+        scratch = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device=dev)
+        cev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.cold_steps)]
+        fev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.cold_steps)]
+        for i in range(args.cold_steps):
+            scratch.fill_(i & 0xff)
+            cev[i][0].record(stream)
+            step(ffn_ev=fev[i])
+            cev[i][1].record(stream)
+        torch.cuda.synchronize()
+        cold = {"steps": args.cold_steps,
+                "step_us": spread(np.array([a.elapsed_time(b) for a, b in cev]) * 1e3),
+                "expert_ffn_us": spread(np.array([a.elapsed_time(b) for a, b in fev]) * 1e3),
+                "note": "512 MiB written before each step, outside the events"}
+        del scratch
 
     # stage breakdown from a separate, untimed pass (its events add gaps between calls)
     nbrk = min(args.steps, 10)
@@ -335,8 +365,11 @@ def main():
                       "note": "separate untimed pass with events between calls" +
                               ("; top-1: the combine is part of the expert step" if top1_fused else "")},
         "expert_ffn_us_timed": round(ffn_us, 2),
+        "timed_steps_us": {"step": spread(step_each), "expert_ffn": spread(ffn_each)},
         "roofline": roof,
     }
+    if cold is not None:
+        out["cold_cache"] = cold
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.config, args.seed)
     print(json.dumps(out), flush=True)
