@@ -693,15 +693,22 @@ void gemm_bf16_lds(GroupedGemm g) {
     }
 }
 // ------------------------------------------------------------------ fp32 kernel
+//
+// 64 x 64 tiles on the fp32 matrix cores: four waves, each one 32 x 32 block of
+// v_mfma_f32_32x32x2_f32 (lane l supplies A[row l % 32][k l / 32] and B[k l / 32][column
+// l % 32] of a two-wide K step, and ends holding column l % 32 of the block).  K advances
+// 32 at a time through two LDS buffers stored K-major ([k][row], 4 floats of padding),
+// each filled from registers loaded two steps earlier (two register sets take turns), so
+// a step's MFMAs overlap the loads of the next two.  Gathered rows are looked up once.
 
-constexpr int kFBM = 64, kFBN = 64, kFBK = 16;
+constexpr int kFBM = 64, kFBN = 64, kFBK = 32, kFLD = kFBM + 4;
 
 template <int EPI, bool OB>
 __global__ __launch_bounds__(kThreads) void gemm_f32(GroupedGemm g) {
     constexpr int NB = (EPI == kEpiSwiglu) ? 2 : 1;
     __shared__ int tstart[kThreads + 1];
-    __shared__ __align__(16) float As[kFBK][kFBM + 4];
-    __shared__ __align__(16) float Bs[NB][kFBK][kFBN + 4];
+    __shared__ __align__(16) float As[2][kFBK][kFLD];
+    __shared__ __align__(16) float Bs[2][NB][kFBK][kFLD];
 
     const int total = tile_prefix<kFBM>(g.offsets, g.E, tstart);
     const int mt = blockIdx.x / g.n_tiles;
@@ -717,69 +724,109 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GroupedGemm g) {
     Bm[0] = static_cast<const float*>(g.b) + e * g.b_estride;
     if (NB > 1) Bm[NB - 1] = static_cast<const float*>(g.b2) + e * g.b_estride;
 
-    const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
-    const int lrow = tid >> 2, lk = (tid & 3) * 4;
-    float acc[NB][4][4] = {};
-    for (int k0 = 0; k0 < g.K; k0 += kFBK) {
-        const bool kv = k0 + lk < g.K;
-        const int64_t ar = row0 + lrow;
-        const float4 a = (ar < row_end && kv) ? *reinterpret_cast<const float4*>(A + source_row(g, ar) * g.K + k0 + lk)
-                                              : make_float4(0.f, 0.f, 0.f, 0.f);
-        As[lk + 0][lrow] = a.x;
-        As[lk + 1][lrow] = a.y;
-        As[lk + 2][lrow] = a.z;
-        As[lk + 3][lrow] = a.w;
+    // loader: thread t brings rows t / 8 and t / 8 + 32, K values 4 (t % 8) .. + 3 of the step
+    // (K % 4 == 0, so a float4 never straddles the end of K)
+    const int tid = threadIdx.x;
+    const int lrow = tid >> 3, lk = (tid & 7) * 4;
+    const float* arow[2];  // this thread's two activation rows (null: past the segment)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-            const int n = n0 + lrow;
-            const float4 b = (n < g.N && kv)
-                                 ? *reinterpret_cast<const float4*>(Bm[nb] + static_cast<int64_t>(n) * g.K + k0 + lk)
-                                 : make_float4(0.f, 0.f, 0.f, 0.f);
-            Bs[nb][lk + 0][lrow] = b.x;
-            Bs[nb][lk + 1][lrow] = b.y;
-            Bs[nb][lk + 2][lrow] = b.z;
-            Bs[nb][lk + 3][lrow] = b.w;
-        }
-        __syncthreads();
+    for (int h = 0; h < 2; ++h) {
+        const int64_t ar = row0 + lrow + 32 * h;
+        arow[h] = ar < row_end ? A + source_row(g, ar) * g.K : nullptr;
+    }
+    struct Regs {
+        float4 a[2], b[NB][2];
+    };
+    auto gload = [&](Regs& R, int kt) {
+        const int k = kt * kFBK + lk;
+        const bool kv = k < g.K;
 #pragma unroll
-        for (int kk = 0; kk < kFBK; ++kk) {
-            const float4 av = *reinterpret_cast<const float4*>(&As[kk][ty * 4]);
-            const float ar4[4] = {av.x, av.y, av.z, av.w};
+        for (int h = 0; h < 2; ++h) {
+            R.a[h] = (arow[h] && kv) ? *reinterpret_cast<const float4*>(arow[h] + k) : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) {
-                const float4 bv = *reinterpret_cast<const float4*>(&Bs[nb][kk][tx * 4]);
-                const float br4[4] = {bv.x, bv.y, bv.z, bv.w};
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) acc[nb][i][j] = fmaf(ar4[i], br4[j], acc[nb][i][j]);
+                const int n = n0 + lrow + 32 * h;
+                R.b[nb][h] = (n < g.N && kv)
+                                 ? *reinterpret_cast<const float4*>(Bm[nb] + static_cast<int64_t>(n) * g.K + k)
+                                 : make_float4(0.f, 0.f, 0.f, 0.f);
             }
         }
+    };
+    auto sstore = [&](const Regs& R, int buf) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int r = lrow + 32 * h;
+            As[buf][lk + 0][r] = R.a[h].x;
+            As[buf][lk + 1][r] = R.a[h].y;
+            As[buf][lk + 2][r] = R.a[h].z;
+            As[buf][lk + 3][r] = R.a[h].w;
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+                Bs[buf][nb][lk + 0][r] = R.b[nb][h].x;
+                Bs[buf][nb][lk + 1][r] = R.b[nb][h].y;
+                Bs[buf][nb][lk + 2][r] = R.b[nb][h].z;
+                Bs[buf][nb][lk + 3][r] = R.b[nb][h].w;
+            }
+        }
+    };
+
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int l32 = lane & 31, lhi = lane >> 5;
+    f32x16_t acc[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
+
+    const int nk = (g.K + kFBK - 1) / kFBK;
+    // step kt: MFMAs on LDS buffer kt % 2; register set `next` holds step kt + 1 and goes to
+    // the other buffer after them (that buffer was last read before the previous step's
+    // barrier), then takes the loads of step kt + 3
+    auto step = [&](int kt, Regs& next) {
+        const int buf = kt & 1;
+#pragma unroll
+        for (int ks = 0; ks < kFBK / 2; ++ks) {
+            const float a = As[buf][2 * ks + lhi][wm * 32 + l32];
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+                acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, Bs[buf][nb][2 * ks + lhi][wn * 32 + l32], acc[nb],
+                                                               0, 0, 0);
+        }
+        if (kt + 1 < nk) sstore(next, buf ^ 1);
         __syncthreads();
+        if (kt + 3 < nk) gload(next, kt + 3);
+    };
+    Regs r0, r1;
+    gload(r0, 0);
+    sstore(r0, 0);
+    if (nk > 1) gload(r1, 1);
+    if (nk > 2) gload(r0, 2);
+    __syncthreads();
+    int kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
+        step(kt, r1);      // r1 holds step kt + 1, then loads kt + 3
+        step(kt + 1, r0);  // r0 holds step kt + 2, then loads kt + 4
     }
-    const int n = n0 + tx * 4;
+    if (kt < nk) step(kt, r1);
+
+    // epilogue: register r holds row 8 (r / 4) + 4 lhi + r % 4 of the wave's block; for a
+    // fixed r the 32 lanes of a half-wave store 32 consecutive columns
+    const int n = n0 + wn * 32 + l32;
     if (n >= g.N) return;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        int64_t row = row0 + ty * 4 + i;
-        if (row >= row_end) break;
+    for (int r = 0; r < 16; ++r) {
+        int64_t row = row0 + wm * 32 + 8 * (r >> 2) + 4 * lhi + (r & 3);
+        if (row >= row_end) continue;
         float scale = 1.f;
         if (g.scatter) {
             const int64_t src = g.scatter[row];
             row = src < 0 ? 0 : (src >= g.c_rows ? g.c_rows - 1 : src);
             scale = g.scatter_w[row];
         }
-        float v[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = scale * epilogue<EPI>(acc[0][i][j], acc[NB - 1][i][j]);
-        if (OB) {
-            uint2 q;
-            q.x = pack_bf16x2(v[0], v[1]);
-            q.y = pack_bf16x2(v[2], v[3]);
-            *reinterpret_cast<uint2*>(static_cast<bf16_t*>(g.c) + row * g.ldc + n) = q;
-        } else {
-            *reinterpret_cast<float4*>(static_cast<float*>(g.c) + row * g.ldc + n) = make_float4(v[0], v[1], v[2], v[3]);
-        }
+        const float v = scale * epilogue<EPI>(acc[0][r], acc[NB - 1][r]);
+        if (OB) static_cast<bf16_t*>(g.c)[row * g.ldc + n] = f32_to_bf16(v);
+        else static_cast<float*>(g.c)[row * g.ldc + n] = v;
     }
 }
 
