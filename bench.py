@@ -15,6 +15,13 @@ write N bytes) that calibrates the counter:
       --no-cpu-baseline --steps 3 --warmup 1 --copy-probe-mib 256
   (the same with WRITE_SIZE into DIR_W)
   python bench.py --config c2 --summarize-counters DIR_F DIR_W   # -> profiles/ffn_traffic_c2.json
+
+MFMA work and busy fraction of the same kernels come from one more counter run:
+
+  rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_VALU_MFMA_MOPS_F32 SQ_VALU_MFMA_BUSY_CYCLES \
+      GRBM_GUI_ACTIVE --output-format csv -d DIR -o run -- python3 bench.py --config c4 \
+      --no-cpu-baseline --steps 3 --warmup 1
+  python bench.py --config c4 --summarize-mfma DIR                # -> profiles/mfma_c4.json
 """
 from __future__ import annotations
 
@@ -22,6 +29,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -99,6 +107,53 @@ def summarize_counters(config: str, fetch_dir: str, write_dir: str, probe_mib: i
            "write_bytes_per_launch": {k: round(v) for k, v in write.items()},
            "hbm_bytes_per_call": round(sum(fetch.values()) + sum(write.values()))}
     path = os.path.join(ROOT, "profiles", f"ffn_traffic_{config}.json")
+    with open(path, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps(rec, indent=1))
+
+
+MFMA_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_INSTS_VALU_MFMA_MOPS_F32", "SQ_VALU_MFMA_BUSY_CYCLES",
+                 "GRBM_GUI_ACTIVE")
+
+
+def summarize_mfma(config: str, pmc_dir: str, simds: int = 1024, xcds: int = 8):
+    """MFMA work and busy fraction of the expert-FFN launches from one rocprofv3 counter run
+    (--pmc with MFMA_COUNTERS), beside the algorithmic flops of the same launches.
+
+    Counter flops = MFMA ops x 512.  Busy = SQ_VALU_MFMA_BUSY_CYCLES summed over the SIMDs /
+    (GRBM_GUI_ACTIVE of one XCD x SIMDs); GRBM_GUI_ACTIVE comes summed over the XCDs."""
+    import csv
+    import glob
+    per = {}
+    for f in glob.glob(os.path.join(pmc_dir, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            k = r["Kernel_Name"]
+            if "gemm_bf16" not in k and "gemm_f32" not in k:
+                continue
+            per.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    if not per:
+        raise SystemExit(f"{pmc_dir}: no expert-FFN launches")
+    cfg = synth.CONFIGS[config]
+    n_up = 2 if cfg.act == "swiglu" else 1
+    alg = {"up": 2.0 * n_up * cfg.A * cfg.h * cfg.f, "down": 2.0 * cfg.A * cfg.h * cfg.f}
+    out = {}
+    for k, cs in per.items():
+        m = {c: float(np.mean(v)) for c, v in cs.items()}
+        flops = (m.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) + m.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0.0)) * 512
+        # the down-projection is the one without an activation epilogue (template argument 3)
+        which = "down" if re.search(r"<(?:[^>]*, )?3, (?:true|false)>", k) else "up"
+        busy = m["SQ_VALU_MFMA_BUSY_CYCLES"] / (m["GRBM_GUI_ACTIVE"] / xcds * simds)
+        out[k] = {"matrix": which, "counter_flops": round(flops), "algorithmic_flops": round(alg[which]),
+                  "counter_over_algorithmic": round(flops / alg[which], 4), "mfma_busy": round(busy, 4)}
+    cmd = (f"rocprofv3 --pmc {' '.join(MFMA_COUNTERS)} --output-format csv -d {pmc_dir} -o run -- python3 bench.py "
+           f"--config {config} --no-cpu-baseline --steps 3 --warmup 1")
+    rec = {"config": config, "ffn_source_hash": ffn_source_hash(),
+           "commands": [cmd, f"python bench.py --config {config} --summarize-mfma {pmc_dir}"],
+           "note": "per launch, averaged over the run's launches; counter flops include the MFMAs of padded rows "
+                   "in 32-row blocks that hold a valid row; busy is the MFMA pipes' busy fraction over the "
+                   "launch, against the clock the kernel ran at",
+           "launches": out}
+    path = os.path.join(ROOT, "profiles", f"mfma_{config}.json")
     with open(path, "w") as fh:
         json.dump(rec, fh, indent=1)
     print(json.dumps(rec, indent=1))
@@ -199,6 +254,7 @@ def main():
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run an untimed plain copy of this size first (counter calibration)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--summarize-mfma", metavar="PMC_DIR")
     ap.add_argument("--unfused-gather", action="store_true",
                     help="write x_perm in the dispatch step instead of gathering rows in the expert step")
     ap.add_argument("--ablation", action="store_true",
@@ -206,6 +262,9 @@ def main():
     args = ap.parse_args()
     if args.summarize_counters:
         summarize_counters(args.config, *args.summarize_counters, probe_mib=args.copy_probe_mib or 256)
+        return
+    if args.summarize_mfma:
+        summarize_mfma(args.config, args.summarize_mfma)
         return
     if args.ablation:
         ablation_per_expert(args.seed, reps=max(args.steps // 5, 5), experts=(8, 16, 32, 64, 128, 256))
