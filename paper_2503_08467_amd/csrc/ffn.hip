@@ -373,11 +373,64 @@ struct TileRows {
     int e;
 };
 
+// The row-tile table (first row tile of every expert): in LDS, written by tile_prefix ...
+struct LdsTiles {
+    const int* tstart;
+    int E;
+    __device__ __forceinline__ int find(int mt) const { return find_expert(tstart, E, mt); }
+    __device__ __forceinline__ int start(int e) const { return tstart[e]; }
+};
+
+// ... or in registers, one copy per wave (for kernels whose LDS is all stage buffers): lane l
+// holds the first row tile of experts 4 l .. 4 l + 3.  Every lane of the wave must call.
 template <int BM>
-__device__ __forceinline__ TileRows tile_rows(const GroupedGemm& g, const int* tstart, int mt) {
+struct RegTiles {
+    int ex[4];
+    int E, total;
+    __device__ __forceinline__ void build(const int32_t* __restrict__ offsets, int num_experts) {
+        static_assert(MOE_MAX_EXPERTS == 4 * 64, "four experts per lane of one wave");
+        E = num_experts;
+        const int lane = threadIdx.x & 63;
+        int run = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int e = lane * 4 + i;
+            const int cnt = (e < E) ? offsets[e + 1] - offsets[e] : 0;
+            ex[i] = run;
+            run += cnt > 0 ? (cnt + BM - 1) / BM : 0;
+        }
+        int incl = run;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int t = __shfl_up(incl, o, 64);
+            if (lane >= o) incl += t;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ex[i] += incl - run;
+        total = __builtin_amdgcn_readfirstlane(__shfl(incl, 63, 64));
+    }
+    // largest expert whose first row tile is <= mt (the table is non-decreasing)
+    __device__ __forceinline__ int find(int mt) const {
+        const int lane = threadIdx.x & 63;
+        int c = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) c += (lane * 4 + i < E && ex[i] <= mt) ? 1 : 0;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+        return c - 1;
+    }
+    __device__ __forceinline__ int start(int e) const {
+        const int q = e & 3;
+        const int v = q == 0 ? ex[0] : q == 1 ? ex[1] : q == 2 ? ex[2] : ex[3];
+        return __shfl(v, e >> 2, 64);
+    }
+};
+
+template <int BM, typename Tiles>
+__device__ __forceinline__ TileRows tile_rows(const GroupedGemm& g, const Tiles& tiles, int mt) {
     TileRows t;
-    t.e = __builtin_amdgcn_readfirstlane(find_expert(tstart, g.E, mt));
-    const int first = __builtin_amdgcn_readfirstlane(tstart[t.e]);
+    t.e = __builtin_amdgcn_readfirstlane(tiles.find(mt));
+    const int first = __builtin_amdgcn_readfirstlane(tiles.start(t.e));
     const int64_t seg0 = g.offsets[t.e], seg1 = g.offsets[t.e + 1];
     t.row0 = seg0 + static_cast<int64_t>(mt - first) * BM;
     t.row_end = seg1 < g.rows_max ? seg1 : g.rows_max;
@@ -405,11 +458,11 @@ struct TileGeom {
     int n0, n_base, e;
 };
 
-template <int BM, int BN>
-__device__ __forceinline__ TileGeom tile_geom(const GroupedGemm& g, const int* tstart, int total_m, int L) {
+template <int BM, int BN, typename Tiles>
+__device__ __forceinline__ TileGeom tile_geom(const GroupedGemm& g, const Tiles& tiles, int total_m, int L) {
     int mt, nt;
     tile_coords(L, total_m, g.n_tiles, mt, nt);
-    const TileRows tr = tile_rows<BM>(g, tstart, mt);
+    const TileRows tr = tile_rows<BM>(g, tiles, mt);
     TileGeom t;
     t.e = tr.e;
     t.row0 = tr.row0;
@@ -453,6 +506,7 @@ void gemm_bf16_lds(GroupedGemm g) {
     extern __shared__ __align__(1024) unsigned char smem_raw[];
 
     const int total_m = tile_prefix<BM>(g.offsets, g.E, tstart);
+    const LdsTiles tiles{tstart, g.E};
     const int total = total_m * g.n_tiles;
     const int per = (total + 7) >> 3;
     const int xcd = blockIdx.x & 7, nslot = gridDim.x >> 3;
@@ -491,7 +545,7 @@ void gemm_bf16_lds(GroupedGemm g) {
     int lt = t_first, lk = 0;
     const unsigned char *src_a = nullptr, *src_b0 = nullptr, *src_b1 = nullptr;
     auto set_tile = [&](int L) {
-        const TileGeom t = tile_geom<BM, BN>(g, tstart, total_m, L);
+        const TileGeom t = tile_geom<BM, BN>(g, tiles, total_m, L);
         const int64_t rb = kUp ? 2 * static_cast<int64_t>(g.K) : 64;
         if (kUp && g.gather) {
             // this lane's activation rows come from the gathered source rows (the index
@@ -567,7 +621,7 @@ void gemm_bf16_lds(GroupedGemm g) {
     constexpr bool kAccInAgpr = S::kPerCU == 1;
     int consumed = 0;
     for (int ct = t_first; ct < t_end; ct += nslot) {
-        const TileGeom t = tile_geom<BM, BN>(g, tstart, total_m, ct);
+        const TileGeom t = tile_geom<BM, BN>(g, tiles, total_m, ct);
         // Row blocks of this wave that hold valid rows.  Valid rows start at the tile's first
         // row unless the tile was shifted back at the end of the buffer; then all count.  The
         // count is rounded up to MI / 2 or MI so that three loop bodies cover every case.
@@ -692,6 +746,238 @@ void gemm_bf16_lds(GroupedGemm g) {
         }
     }
 }
+// ------------------------------------------------------------------ bf16 up-projection, paired A stages
+//
+// The up-projection's activations are rows of x (gathered through row_src) or of x_perm,
+// row-major, so the kernel above reads them as 64-byte pieces: half a 128-byte line per
+// stage, the other half a stage later.  This variant (K % 64 == 0) loads 128 bytes of an
+// activation row for two stages at once.  The A side has two 16 KiB slots of 128 rows x
+// 128 bytes (one in use, one filling; chunk c of row r sits at c ^ (r % 8), so the 8 rows
+// that 8 lanes of a fragment read touch fall on 8 different bank groups); the weights keep
+// the three-stage ring of K-blocked 256-row stages.  That is 80 KiB, two workgroups per CU
+// with nothing left over, so the row-tile table is kept in registers.  Even stages issue 4
+// A and 4 B loads per wave, odd stages 4 B loads; the vmcnt waits count them that way.
+// Fragments, MFMA order and epilogue are those of gemm_bf16_lds<128, 256, 32, 3, EPI,
+// true>, and so is every output bit.
+constexpr int kUpASlot = 128 * 128;                       // bytes of one A slot
+constexpr int kUpBSlot = 256 * 64;                        // bytes of one B stage
+constexpr size_t kUpPairBytes = 2 * kUpASlot + 3 * kUpBSlot;  // 80 KiB
+
+template <int EPI>
+__global__ __launch_bounds__(kThreads, 2) void gemm_up_pairs(GroupedGemm g) {
+    constexpr int BM = 128, BW = 256, NS = 3;
+    typedef LdsShape<BM, BW, 32, NS, EPI> S;
+    constexpr int NB = S::kNB, BN = S::kBN, MI = S::kMI, NI = S::kNI, KS = S::kKS;
+    constexpr int kBBase = 2 * kUpASlot;
+    constexpr int LPA = BM / 8 / 4;   // 1 KiB loads per wave of an A pair (8 rows x 128 bytes)
+    constexpr int LPB = BW / 16 / 4;  // 1 KiB loads per wave of a B stage (16 rows x 64 bytes)
+    static_assert(kUpPairBytes <= 80 * 1024, "two workgroups per CU");
+    extern __shared__ __align__(1024) unsigned char smem_raw[];
+
+    RegTiles<BM> tiles;
+    tiles.build(g.offsets, g.E);
+    const int total_m = tiles.total;
+    const int total = total_m * g.n_tiles;
+    const int per = (total + 7) >> 3;
+    const int xcd = blockIdx.x & 7, nslot = gridDim.x >> 3;
+    const int t_end = min(total, (xcd + 1) * per);
+    const int t_first = xcd * per + static_cast<int>(blockIdx.x >> 3);
+    if (t_first >= t_end) return;
+    const int nk = g.K / 32;  // even: the host runs this kernel only for K % 64 == 0
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint32_t lds0 = lds_address(smem_raw);
+    const int a_lim = static_cast<int>(g.rows_max < BM ? g.rows_max : BM) - 1;
+    const int b_lim = (g.N < BN ? g.N : BN) - 1;
+
+    // B: load j fills B rows (4 j + wave) 16 + lane / 4 of a stage, slot lane % 4, with global
+    // chunk slot ^ ((row / 4) % 4); the same for every tile
+    uint32_t voffB[LPB];
+#pragma unroll
+    for (int j = 0; j < LPB; ++j) {
+        const int R = (j * 4 + wave) * 16 + (lane >> 2);
+        const int kc = (lane & 3) ^ ((R >> 2) & 3);
+        voffB[j] = static_cast<uint32_t>(min(R % BN, b_lim)) * 64u + static_cast<uint32_t>(kc * 16);
+    }
+    // A: load j fills A rows (4 j + wave) 8 + lane / 8 of a slot, slot lane % 8, with global
+    // chunk slot ^ (row % 8); set per tile
+    uint32_t voffA[LPA];
+
+    int lt = t_first, lk = 0;
+    const unsigned char *src_a = nullptr, *src_b0 = nullptr, *src_b1 = nullptr;
+    auto set_tile = [&](int L) {
+        const TileGeom t = tile_geom<BM, BN>(g, tiles, total_m, L);
+#pragma unroll
+        for (int j = 0; j < LPA; ++j) {
+            const int R = (j * 4 + wave) * 8 + (lane >> 3);
+            const int c = (lane & 7) ^ (R & 7);
+            // gathered: absolute source row (T h s < 4 GiB is checked by the host); else the
+            // tile's base carries the row offset
+            const int64_t r = g.gather ? source_row(g, t.row_base + min(R, a_lim)) : min(R, a_lim);
+            voffA[j] = static_cast<uint32_t>(r) * static_cast<uint32_t>(2 * g.K) + static_cast<uint32_t>(c * 16);
+        }
+        src_a = uniform_ptr(static_cast<const unsigned char*>(g.a) + (g.gather ? 0 : t.row_base * 2 * g.K));
+        const int64_t boff = (t.e * g.b_estride) * 2 + static_cast<int64_t>(t.n_base) * 64;
+        src_b0 = uniform_ptr(static_cast<const unsigned char*>(g.b) + boff);
+        src_b1 = NB > 1 ? uniform_ptr(static_cast<const unsigned char*>(g.b2) + boff) : src_b0;
+    };
+    int issued = 0;  // stages issued by this wave so far (even at every tile start: nk is even)
+    auto issue_next = [&]() {
+        if (lt >= t_end) return;
+        if ((lk & 1) == 0) {
+            // the next 128 bytes of every activation row: K blocks lk and lk + 1
+            const uint32_t da = lds0 + ((issued >> 1) & 1) * kUpASlot;
+#pragma unroll
+            for (int j = 0; j < LPA; ++j)
+                load_lds16(src_a + static_cast<int64_t>(lk) * 64, voffA[j], da + (j * 4 + wave) * 1024);
+        }
+        const uint32_t db = lds0 + kBBase + (issued % NS) * kUpBSlot;
+        const int64_t kb = static_cast<int64_t>(lk) * g.N * 64;
+#pragma unroll
+        for (int j = 0; j < LPB; ++j)
+            load_lds16(((NB > 1 && j * 4 * 16 >= BN) ? src_b1 : src_b0) + kb, voffB[j], db + (j * 4 + wave) * 1024);
+        ++issued;
+        if (++lk == nk) {
+            lk = 0;
+            lt += nslot;
+            if (lt < t_end) set_tile(lt);
+        }
+    };
+    // wait until stage `st` is in LDS while `newer` later stages stay in flight
+    auto wait_stage = [&](int st, int newer) {
+        if (newer >= 2) wait_vmcnt<LPA + 2 * LPB>();
+        else if (newer == 1 && ((st + 1) & 1) == 0) wait_vmcnt<LPA + LPB>();
+        else if (newer == 1) wait_vmcnt<LPB>();
+        else wait_vmcnt<0>();
+    };
+    set_tile(lt);
+#pragma unroll
+    for (int st = 0; st < NS - 1; ++st) issue_next();
+
+    const int wm = wave >> 1, wn = wave & 1;
+    const int l32 = lane & 31, lhi = lane >> 5;
+    typedef bf16x8_t Frags[MI + NB * NI];
+    // fragments of stage st (its A slot and half of the slot's rows, its B ring slot)
+    auto read_frags = [&](auto nv_tag, int st, int ks, Frags& f) {
+        constexpr int NV = decltype(nv_tag)::value;
+        const unsigned char* sa = smem_raw + ((st >> 1) & 1) * kUpASlot;
+        const int ca = (st & 1) * 4 + 2 * ks + lhi;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            const int R = wm * (BM / 2) + i * 32 + l32;
+            f[i] = *reinterpret_cast<const bf16x8_t*>(sa + R * 128 + ((ca ^ (R & 7)) << 4));
+        }
+        if (NV == 0) return;
+        const unsigned char* sb = smem_raw + kBBase + (st % NS) * kUpBSlot;
+        const int cb = 2 * ks + lhi;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int j = 0; j < NI; ++j) {
+                const int R = nb * BN + wn * (BN / 2) + j * 32 + l32;
+                f[MI + nb * NI + j] = *reinterpret_cast<const bf16x8_t*>(sb + R * 64 + ((cb ^ ((R >> 2) & 3)) << 4));
+            }
+    };
+
+    int consumed = 0;
+    for (int ct = t_first; ct < t_end; ct += nslot) {
+        const TileGeom t = tile_geom<BM, BN>(g, tiles, total_m, ct);
+        int nv = MI;
+        if (t.row_base == t.row0) {
+            const int64_t left = t.row_end - (t.row0 + wm * (BM / 2));
+            nv = left <= 0 ? 0 : (left > (MI / 2) * 32 ? MI : MI / 2);
+        }
+        nv = __builtin_amdgcn_readfirstlane(nv);
+
+        f32x16_t acc[NB][MI][NI];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int i = 0; i < MI; ++i)
+#pragma unroll
+                for (int j = 0; j < NI; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) acc[nb][i][j][r] = 0.f;
+
+        // publish the tile's first stage; after an epilogue its stores share the counter
+        if (ct != t_first) wait_vmcnt<0>();
+        else wait_stage(consumed, issued - consumed - 1);
+        stage_barrier();
+        issue_next();
+
+        auto k_loop = [&](auto nv_tag) {
+            constexpr int NV = decltype(nv_tag)::value;
+            auto mma = [&](const Frags& f) {
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                    for (int j = 0; j < NI; ++j)
+#pragma unroll
+                        for (int i = 0; i < NV; ++i)
+                            acc[nb][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[MI + nb * NI + j], f[i],
+                                                                                    acc[nb][i][j], 0, 0, 0);
+            };
+            Frags f0, f1;
+            read_frags(nv_tag, consumed, 0, f0);
+            for (int ck = 0; ck < nk; ++ck) {
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    Frags& cur = (ks & 1) ? f1 : f0;
+                    Frags& nxt = (ks & 1) ? f0 : f1;
+                    if (ks + 1 < KS) {
+                        read_frags(nv_tag, consumed, ks + 1, nxt);
+                    } else if (ck + 1 < nk) {
+                        wait_lgkm0();
+                        wait_stage(consumed + 1, issued - consumed - 2);
+                        stage_barrier();
+                        issue_next();
+                        read_frags(nv_tag, consumed + 1, 0, nxt);
+                    }
+                    if (NV > 0) {
+                        mma(cur);
+                        interleave_reads<NB * NV * NI, NV + NB * NI>();
+                    }
+                }
+                ++consumed;
+            }
+        };
+        if (nv == MI) k_loop(std::integral_constant<int, MI>());
+        else if (nv > 0) k_loop(std::integral_constant<int, MI / 2>());
+        else k_loop(std::integral_constant<int, 0>());
+
+        // epilogue: as in gemm_bf16_lds (bf16 H, K-blocked)
+        const int64_t row_lo = t.row0 > 0 ? t.row0 : 0;
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+            if (i >= nv) break;
+            const int64_t row = t.row_base + wm * (BM / 2) + i * 32 + l32;
+            const bool row_ok = row >= row_lo && row < t.row_end;
+#pragma unroll
+            for (int j = 0; j < NI; ++j) {
+                const int col0 = t.n_base + wn * (BN / 2) + j * 32 + 4 * lhi;
+                bf16_t* const dst = static_cast<bf16_t*>(g.c) +
+                                    ((static_cast<int64_t>(col0) >> 5) * g.rows_max + row) * 32 + (col0 & 31);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int col = col0 + 8 * q;
+                    float v[4];
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+                        v[c] = epilogue_fast<EPI>(acc[0][i][j][4 * q + c], acc[NB - 1][i][j][4 * q + c]);
+                    if (row_ok && col >= t.n0 && col < g.N) {
+                        uint2 pk;
+                        pk.x = pack_bf16x2(v[0], v[1]);
+                        pk.y = pack_bf16x2(v[2], v[3]);
+                        *reinterpret_cast<uint2*>(dst + 8 * q) = pk;
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+        }
+    }
+}
+
 // ------------------------------------------------------------------ fp32 kernel
 //
 // 64 x 64 tiles on the fp32 matrix cores: four waves, each one 32 x 32 block of
@@ -907,10 +1193,29 @@ hipError_t run_bf16_lds(GroupedGemm g, int64_t A_max, hipStream_t s) {
 // tiles, one workgroup per CU with 96 KiB of stages: every tile then streams its weights
 // with more bytes in flight instead of a third of the CUs taking a second tile.  Each
 // output element's K sum is the same in either shape.
+template <int EPI>
+hipError_t run_up_pairs(GroupedGemm g, int64_t A_max, hipStream_t s) {
+    static const hipError_t attr =
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_up_pairs<EPI>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kUpPairBytes));
+    if (attr != hipSuccess) return attr;
+    g.n_tiles = static_cast<int>(ceil_div(g.N, LdsShape<128, 256, 32, 3, EPI>::kBN));
+    const int64_t tiles = row_tile_bound(A_max, g.E, 128) * g.n_tiles;
+    if (tiles == 0) return hipSuccess;
+    const int64_t blocks = round_up(std::min<int64_t>(tiles, 2 * static_cast<int64_t>(device_cus())), 8);
+    hipLaunchKernelGGL((gemm_up_pairs<EPI>), dim3(static_cast<unsigned>(blocks)), dim3(kThreads), kUpPairBytes, s,
+                       g);
+    return hipGetLastError();
+}
+
 template <int EPI, bool OB>
 hipError_t run_bf16_best(GroupedGemm g, int64_t A_max, hipStream_t s) {
     constexpr bool kUp = EPI != kEpiNone;
     if constexpr (kUp) {
+        // activation rows in 128-byte pieces when K allows it (see gemm_up_pairs)
+        if constexpr (OB) {
+            if (g.K % 64 == 0) return run_up_pairs<EPI>(g, A_max, s);
+        }
         if (g.K % 32 == 0) return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);
         return run_bf16<EPI, OB, true>(g, A_max, s);
     } else {
