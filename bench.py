@@ -68,6 +68,11 @@ def measured_traffic(config: str):
     return rec.get("hbm_bytes_per_call")
 
 
+def is_ffn_kernel(name: str) -> bool:
+    """The grouped-GEMM kernels of the expert step (up- and down-projection)."""
+    return any(k in name for k in ("gemm_bf16", "gemm_up_pairs", "gemm_f32"))
+
+
 def summarize_counters(config: str, fetch_dir: str, write_dir: str, probe_mib: int):
     """Per-call HBM bytes of the expert-FFN launches from two rocprofv3 counter runs.
 
@@ -86,7 +91,7 @@ def summarize_counters(config: str, fetch_dir: str, write_dir: str, probe_mib: i
                     continue
                 per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]) * 1024.0)
         probe = [v for k, vs in per.items() if "neg" in k for v in vs]
-        gemm = {k: float(np.mean(v)) for k, v in per.items() if "gemm_bf16" in k or "gemm_f32" in k}
+        gemm = {k: float(np.mean(v)) for k, v in per.items() if is_ffn_kernel(k)}
         if not probe or not gemm:
             raise SystemExit(f"{d}: missing copy probe or expert-FFN launches for {counter}")
         factor = known / float(np.median(probe))
@@ -128,7 +133,7 @@ def summarize_mfma(config: str, pmc_dir: str, simds: int = 1024, xcds: int = 8):
     for f in glob.glob(os.path.join(pmc_dir, "**", "*counter_collection.csv"), recursive=True):
         for r in csv.DictReader(open(f)):
             k = r["Kernel_Name"]
-            if "gemm_bf16" not in k and "gemm_f32" not in k:
+            if not is_ffn_kernel(k):
                 continue
             per.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
     if not per:
