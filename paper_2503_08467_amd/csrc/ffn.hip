@@ -334,24 +334,27 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16(GroupedGemm g) {
 // the MFMA's first operand, so each lane ends up holding 4 consecutive output columns of
 // one row (one 8- or 16-byte store per group).  K must be a multiple of 32.
 
-template <int BM, int BW, int BK, int NS, int EPI>
+// WN: waves along the tile's columns (the waves are 2 x WN; 4 or 8 per workgroup).
+template <int BM, int BW, int BK, int NS, int EPI, int WN = 2>
 struct LdsShape {
     static constexpr bool kDual = (EPI == kEpiSwiglu);
     static constexpr int kNB = kDual ? 2 : 1;
     static constexpr int kBN = BW / kNB;          // output columns per tile
-    static constexpr int kMI = BM / 64;           // 32-row blocks per wave (2 x 2 waves)
-    static constexpr int kNI = kBN / 64;          // 32-column blocks per wave per matrix
+    static constexpr int kWaves = 2 * WN;
+    static constexpr int kThreadsWG = 64 * kWaves;
+    static constexpr int kMI = BM / 64;           // 32-row blocks per wave (BM / 2 rows)
+    static constexpr int kNI = kBN / (32 * WN);   // 32-column blocks per wave per matrix
     static constexpr int kCPR = BK / 8;           // 16-byte chunks per LDS row
     static constexpr int kRPI = 64 / kCPR;        // LDS rows per 1 KiB wave load
     static constexpr int kRows = BM + BW;         // LDS rows per stage
-    static constexpr int kLPW = kRows / kRPI / 4;  // 1 KiB loads per wave per stage
+    static constexpr int kLPW = kRows / kRPI / kWaves;  // 1 KiB loads per wave per stage
     static constexpr int kKS = BK / 16;           // MFMA K steps per stage
     static constexpr int kSwzShift = (kCPR == 8) ? 1 : 2;  // rows sharing a 256-byte bank line
     static constexpr size_t kBytes = (size_t)NS * kRows * BK * 2;
     static constexpr int kPerCU = (kBytes <= 80 * 1024) ? 2 : 1;  // workgroups per CU
-    static_assert(kMI >= 1 && kNI >= 1, "tile too small for 2 x 2 waves of 32 x 32 blocks");
-    static_assert(kRows % (kRPI * 4) == 0, "stage rows must split evenly over the waves");
-    static_assert(BM % (4 * kRPI) == 0 && kBN % (4 * kRPI) == 0, "a wave load carries one kind of row");
+    static_assert(kMI >= 1 && kNI >= 1 && kBN % (32 * WN) == 0, "tile too small for the waves' 32 x 32 blocks");
+    static_assert(kRows % (kRPI * kWaves) == 0, "stage rows must split evenly over the waves");
+    static_assert(BM % (kWaves * kRPI) == 0 && kBN % (kWaves * kRPI) == 0, "a wave load carries one kind of row");
     static_assert(BK == 32, "the K-blocked operands come in blocks of 32");
 };
 
@@ -493,15 +496,16 @@ __device__ __forceinline__ TileGeom tile_geom(const GroupedGemm& g, const Tiles&
 //
 // The activation epilogues belong to the up-projection (A = x_perm row-major, C = H
 // K-blocked); the plain one to the down-projection (A = H K-blocked, C = y_perm row-major).
-template <int BM, int BW, int BK, int NS, int EPI, bool OB>
-__global__ __launch_bounds__(kThreads, (LdsShape<BM, BW, BK, NS, EPI>::kPerCU))
+template <int BM, int BW, int BK, int NS, int EPI, bool OB, int WN = 2>
+__global__ __launch_bounds__((LdsShape<BM, BW, BK, NS, EPI, WN>::kThreadsWG),
+                             (LdsShape<BM, BW, BK, NS, EPI, WN>::kPerCU))
 void gemm_bf16_lds(GroupedGemm g) {
-    typedef LdsShape<BM, BW, BK, NS, EPI> S;
+    typedef LdsShape<BM, BW, BK, NS, EPI, WN> S;
     constexpr bool kUp = EPI != kEpiNone;
     constexpr int NB = S::kNB, BN = S::kBN, MI = S::kMI, NI = S::kNI, ROWS = S::kRows, LPW = S::kLPW;
-    constexpr int CPR = S::kCPR, RPI = S::kRPI, SH = S::kSwzShift, KS = S::kKS;
+    constexpr int CPR = S::kCPR, RPI = S::kRPI, SH = S::kSwzShift, KS = S::kKS, NW = S::kWaves;
     constexpr int kStageBytes = ROWS * BK * 2;
-    constexpr int kAJ = BM / (4 * RPI);  // loads per wave per stage that carry activation rows
+    constexpr int kAJ = BM / (NW * RPI);  // loads per wave per stage that carry activation rows
     __shared__ int tstart[kThreads + 1];
     extern __shared__ __align__(1024) unsigned char smem_raw[];
 
@@ -521,7 +525,7 @@ void gemm_bf16_lds(GroupedGemm g) {
     const uint32_t lds0 = __builtin_amdgcn_readfirstlane(
         static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) void*)smem_raw)));
 
-    // Per-lane byte offsets of this wave's loads: load j fills LDS rows (4 j + wave) * RPI
+    // Per-lane byte offsets of this wave's loads: load j fills LDS rows (NW j + wave) * RPI
     // + lane / CPR of a stage, slot lane % CPR, with global chunk slot ^ swz(row).  Rows past
     // a buffer smaller than one tile repeat its last row.
     uint32_t voff[LPW];
@@ -531,7 +535,7 @@ void gemm_bf16_lds(GroupedGemm g) {
         const int b_lim = (g.N < BN ? g.N : BN) - 1;
 #pragma unroll
         for (int j = 0; j < LPW; ++j) {
-            const int R = (j * 4 + wave) * RPI + r_lane;
+            const int R = (j * NW + wave) * RPI + r_lane;
             const int kc = c_lane ^ ((R >> SH) & (CPR - 1));
             int r;
             if (j < kAJ) r = min(R, a_lim);
@@ -554,7 +558,7 @@ void gemm_bf16_lds(GroupedGemm g) {
             const int a_lim = static_cast<int>(g.rows_max < BM ? g.rows_max : BM) - 1;
 #pragma unroll
             for (int j = 0; j < kAJ; ++j) {
-                const int R = (j * 4 + wave) * RPI + r_lane;
+                const int R = (j * NW + wave) * RPI + r_lane;
                 const int kc = c_lane ^ ((R >> SH) & (CPR - 1));
                 const int64_t src = source_row(g, t.row_base + min(R, a_lim));
                 voff[j] = static_cast<uint32_t>(src) * static_cast<uint32_t>(2 * g.K) + static_cast<uint32_t>(kc * 16);
@@ -577,8 +581,8 @@ void gemm_bf16_lds(GroupedGemm g) {
         const int64_t kb = static_cast<int64_t>(lk) * g.N * 64;
 #pragma unroll
         for (int j = 0; j < LPW; ++j) {
-            const unsigned char* base = j < kAJ ? src_a + ka : ((NB > 1 && (j - kAJ) * 4 * RPI >= BN) ? src_b1 : src_b0) + kb;
-            load_lds16(base, voff[j], dst + (j * 4 + wave) * RPI * CPR * 16);
+            const unsigned char* base = j < kAJ ? src_a + ka : ((NB > 1 && (j - kAJ) * NW * RPI >= BN) ? src_b1 : src_b0) + kb;
+            load_lds16(base, voff[j], dst + (j * NW + wave) * RPI * CPR * 16);
         }
         ++issued;
         if (++lk == nk) {
@@ -594,7 +598,7 @@ void gemm_bf16_lds(GroupedGemm g) {
     // ---- fragments: A block i = activation rows wm*BM/2 + 32 i + l32, B block (nb, j) =
     // weight rows BM + nb*BN + wn*BN/2 + 32 j + l32; K chunk 2 ks + lhi of the stage.  Only
     // the first NV row blocks of the wave are read (the rest hold no valid row).
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WN, wn = wave % WN;
     const int l32 = lane & 31, lhi = lane >> 5;
     typedef bf16x8_t Frags[MI + NB * NI];
     auto read_frags = [&](auto nv_tag, int stage_slot, int ks, Frags& f) {
@@ -611,7 +615,7 @@ void gemm_bf16_lds(GroupedGemm g) {
         for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
             for (int j = 0; j < NI; ++j) {
-                const int R = BM + nb * BN + wn * (BN / 2) + j * 32 + l32;
+                const int R = BM + nb * BN + wn * (BN / WN) + j * 32 + l32;
                 f[MI + nb * NI + j] =
                     *reinterpret_cast<const bf16x8_t*>(st + R * (2 * BK) + ((ch ^ ((R >> SH) & (CPR - 1))) << 4));
             }
@@ -716,7 +720,7 @@ void gemm_bf16_lds(GroupedGemm g) {
             for (int j = 0; j < NI; ++j) {
                 // this lane's first column in the block; the 4-column groups col .. col + 3
                 // never cross a 32-column block (K-blocked H) nor the end of a row (N % 4 == 0)
-                const int col0 = t.n_base + wn * (BN / 2) + j * 32 + 4 * lhi;
+                const int col0 = t.n_base + wn * (BN / WN) + j * 32 + 4 * lhi;
                 OutT* const dst = static_cast<OutT*>(g.c) +
                                   (kUp ? ((static_cast<int64_t>(col0) >> 5) * g.rows_max + row) * 32 + (col0 & 31)
                                        : row * g.ldc + col0);
@@ -1161,13 +1165,13 @@ int device_cus() {
     return cus;
 }
 
-template <int BM, int BW, int BK, int NS, int EPI, bool OB>
+template <int BM, int BW, int BK, int NS, int EPI, bool OB, int WN = 2>
 hipError_t run_bf16_lds(GroupedGemm g, int64_t A_max, hipStream_t s) {
-    typedef LdsShape<BM, BW, BK, NS, EPI> S;
+    typedef LdsShape<BM, BW, BK, NS, EPI, WN> S;
     constexpr size_t lds = S::kBytes;
     constexpr int per_cu = S::kPerCU;
     static const hipError_t attr = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&gemm_bf16_lds<BM, BW, BK, NS, EPI, OB>),
+        reinterpret_cast<const void*>(&gemm_bf16_lds<BM, BW, BK, NS, EPI, OB, WN>),
         hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
     if (attr != hipSuccess) return attr;
     g.n_tiles = static_cast<int>(ceil_div(g.N, S::kBN));
@@ -1175,8 +1179,8 @@ hipError_t run_bf16_lds(GroupedGemm g, int64_t A_max, hipStream_t s) {
     if (tiles == 0) return hipSuccess;
     // persistent grid: at most per_cu workgroups per CU, a multiple of the 8 XCDs
     const int64_t blocks = round_up(std::min<int64_t>(tiles, static_cast<int64_t>(per_cu) * device_cus()), 8);
-    hipLaunchKernelGGL((gemm_bf16_lds<BM, BW, BK, NS, EPI, OB>), dim3(static_cast<unsigned>(blocks)), dim3(kThreads),
-                       lds, s, g);
+    hipLaunchKernelGGL((gemm_bf16_lds<BM, BW, BK, NS, EPI, OB, WN>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(S::kThreadsWG), lds, s, g);
     return hipGetLastError();
 }
 
@@ -1191,8 +1195,10 @@ hipError_t run_bf16_lds(GroupedGemm g, int64_t A_max, hipStream_t s) {
 // When the down-projection's tiles fit on the CUs in one round even 384 columns wide (few
 // rows, e.g. a top-1 layer of a few thousand tokens or a decode batch), it runs 128 x 384
 // tiles, one workgroup per CU with 96 KiB of stages: every tile then streams its weights
-// with more bytes in flight instead of a third of the CUs taking a second tile.  Each
-// output element's K sum is the same in either shape.
+// with more bytes in flight instead of a third of the CUs taking a second tile.  That
+// workgroup has 8 waves (2 x 4, each 64 x 96), two per SIMD, so that one wave's LDS reads,
+// loads and barrier waits overlap the other's MFMAs.  Each output element's K sum is the
+// same in any of these shapes.
 template <int EPI>
 hipError_t run_up_pairs(GroupedGemm g, int64_t A_max, hipStream_t s) {
     static const hipError_t attr =
@@ -1221,7 +1227,7 @@ hipError_t run_bf16_best(GroupedGemm g, int64_t A_max, hipStream_t s) {
     } else {
         if (g.K % 32 != 0) return hipErrorInvalidValue;  // not reachable through the C ABI (fp % 128 == 0)
         if (g.N >= 384 && row_tile_bound(A_max, g.E, 128) * ceil_div(g.N, 384) <= device_cus())
-            return run_bf16_lds<128, 384, 32, 3, EPI, OB>(g, A_max, s);
+            return run_bf16_lds<128, 384, 32, 3, EPI, OB, 4>(g, A_max, s);
         return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);
     }
 }
