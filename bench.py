@@ -73,6 +73,12 @@ def is_ffn_kernel(name: str) -> bool:
     return any(k in name for k in ("gemm_bf16", "gemm_up_pairs", "gemm_f32"))
 
 
+def ffn_matrix(name: str) -> str:
+    """"down" for the down-projection launch (epilogue template argument 3, no activation),
+    else "up"."""
+    return "down" if re.search(r"<(?:[^>]*, )?3, (?:true|false)(?:, \d+)?>", name) else "up"
+
+
 def summarize_counters(config: str, fetch_dir: str, write_dir: str, probe_mib: int):
     """Per-call HBM bytes of the expert-FFN launches from two rocprofv3 counter runs.
 
@@ -145,8 +151,7 @@ def summarize_mfma(config: str, pmc_dir: str, simds: int = 1024, xcds: int = 8):
     for k, cs in per.items():
         m = {c: float(np.mean(v)) for c, v in cs.items()}
         flops = (m.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) + m.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0.0)) * 512
-        # the down-projection is the one without an activation epilogue (template argument 3)
-        which = "down" if re.search(r"<(?:[^>]*, )?3, (?:true|false)>", k) else "up"
+        which = ffn_matrix(k)
         busy = m["SQ_VALU_MFMA_BUSY_CYCLES"] / (m["GRBM_GUI_ACTIVE"] / xcds * simds)
         out[k] = {"matrix": which, "counter_flops": round(flops), "algorithmic_flops": round(alg[which]),
                   "counter_over_algorithmic": round(flops / alg[which], 4), "mfma_busy": round(busy, 4)}

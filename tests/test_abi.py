@@ -146,3 +146,18 @@ def test_python_binding_refuses_cpu_tensors():
     x = torch.zeros(4, 64, dtype=torch.bfloat16)
     with pytest.raises(ValueError, match="GPU tensor"):
         moe.route(x, torch.zeros(8, 64, dtype=torch.bfloat16), 1)
+
+
+def test_bench_names_the_expert_step_kernels():
+    # the counter summaries pick the expert-step launches out of a profile by name
+    import bench
+    up = ["void moe::(anonymous namespace)::gemm_up_pairs<0>(moe::(anonymous namespace)::GroupedGemm)",
+          "void moe::(anonymous namespace)::gemm_bf16_lds<128, 256, 32, 3, 2, true, 2>(moe::(anonymous namespace)::GroupedGemm)",
+          "void moe::(anonymous namespace)::gemm_f32<0, false>(moe::(anonymous namespace)::GroupedGemm)"]
+    down = ["void moe::(anonymous namespace)::gemm_bf16_lds<128, 384, 32, 3, 3, true, 4>(moe::(anonymous namespace)::GroupedGemm)",
+            "void moe::(anonymous namespace)::gemm_bf16_lds<128, 256, 32, 3, 3, false, 2>(moe::(anonymous namespace)::GroupedGemm)",
+            "void moe::(anonymous namespace)::gemm_f32<3, true>(moe::(anonymous namespace)::GroupedGemm)"]
+    assert all(bench.is_ffn_kernel(n) for n in up + down)
+    assert not bench.is_ffn_kernel("void moe::(anonymous namespace)::route_lds_kernel<1>(unsigned short const*)")
+    assert [bench.ffn_matrix(n) for n in up] == ["up"] * 3
+    assert [bench.ffn_matrix(n) for n in down] == ["down"] * 3
