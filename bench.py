@@ -44,7 +44,7 @@ PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_F32_TFLOPS = 157.3
 FFN_SOURCES = ["paper_2503_08467_amd/csrc/ffn.hip", "paper_2503_08467_amd/csrc/common.h",
-               "paper_2503_08467_amd/csrc/lds_dma.h"]
+               "paper_2503_08467_amd/csrc/lds_dma.h", "paper_2503_08467_amd/csrc/kernels.h"]
 
 
 def ffn_source_hash() -> str:
@@ -69,13 +69,16 @@ def measured_traffic(config: str):
 
 
 def is_ffn_kernel(name: str) -> bool:
-    """The grouped-GEMM kernels of the expert step (up- and down-projection)."""
-    return any(k in name for k in ("gemm_bf16", "gemm_up_pairs", "gemm_f32"))
+    """The kernels of the expert step: the grouped GEMMs (up- and down-projection) and, for
+    small bf16 calls whose down-projection splits K, the sum of its parts."""
+    return any(k in name for k in ("gemm_bf16", "gemm_up_pairs", "gemm_f32", "split_reduce"))
 
 
 def ffn_matrix(name: str) -> str:
-    """"down" for the down-projection launch (epilogue template argument 3, no activation),
-    else "up"."""
+    """"down" for the down-projection launches (epilogue template argument 3, no activation;
+    the sum of its K parts), else "up"."""
+    if "split_reduce" in name:
+        return "down"
     return "down" if re.search(r"<(?:[^>]*, )?3, (?:true|false)(?:, \d+)?>", name) else "up"
 
 
@@ -414,7 +417,8 @@ def main():
              "frac": round(achieved_tflops / peak_tf, 4)})
     roof["traffic"] = measured_traffic(args.config)
     roof["kernel"] = ("moe_expert_ffn_shard" + ("_top1" if top1_fused else "" if args.unfused_gather else "_gather") +
-                      " (grouped GEMM1+act and GEMM2, one launch each)")
+                      " (grouped GEMM1+act and GEMM2, one launch each; calls of at most 512 bf16 rows"
+                      " add one launch that sums the K parts of GEMM2)")
     roof["algorithmic"] = {"bytes": ffn_bytes, "flops": ffn_flops, "touched_experts": touched,
                            "mfma_util": round(achieved_tflops / peak_tf, 4),
                            "hbm_frac": round(achieved_gbs / PEAK_HBM_GBS, 4)}

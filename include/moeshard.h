@@ -129,7 +129,9 @@ moe_status moe_pack_weights(const void *w1, const void *w3, const void *w2, int3
                             moe_dtype wdt, void *packed, size_t packed_bytes,
                             hipStream_t stream);
 
-/* Bytes of workspace moe_expert_ffn_shard needs (the activated inner rows, A_max x fp). */
+/* Bytes of workspace moe_expert_ffn_shard needs: the activated inner rows (A_max x fp) and,
+ * for bf16 calls with A_max <= 512, fp32 partial sums of the second product (its K is
+ * then split into up to 8 parts so that few rows still occupy the whole GPU). */
 size_t moe_ffn_workspace_size(int64_t A_max, int32_t E, int64_t h, int64_t f, moe_act act,
                               moe_dtype dt);
 
@@ -138,7 +140,10 @@ size_t moe_ffn_workspace_size(int64_t A_max, int32_t E, int64_t h, int64_t f, mo
  *     y_perm[p] = act(x_perm[p] . W1_e^g) . W2_e^g        (shard g = the packed slice)
  * computed with bf16 MFMA and fp32 accumulation (dt = MOE_BF16) or fp32 arithmetic
  * (dt = MOE_F32).  The activated row is rounded to dt before the second product.  One
- * launch per matmul regardless of E; the per-expert counts are read on the device.
+ * launch per matmul regardless of E; the per-expert counts are read on the device.  A small
+ * bf16 call (A_max <= 512) sums the second product's K in parts, each part in fp32, the
+ * parts added in a fixed order by one more launch; the split depends only on A_max and f,
+ * so results are deterministic and every entry point agrees bit for bit on one call.
  *   x_perm  [A, h] dtype dt, grouped rows from moe_dispatch
  *   offsets [E+1] int32, device; offsets[E] must not exceed A_max
  *   A_max   host-known upper bound of offsets[E] (normally T*k); sizes the launch

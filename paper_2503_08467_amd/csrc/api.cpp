@@ -124,12 +124,12 @@ moe_status moe_pack_weights(const void* w1, const void* w3, const void* w2, int3
 
 size_t moe_ffn_workspace_size(int64_t A_max, int32_t E, int64_t h, int64_t f, moe_act act, moe_dtype dt) {
     (void)E;
-    (void)h;
     (void)act;
-    if (A_max < 0 || f < 1 || !valid_dtype(dt)) return 0;
-    return align_up(static_cast<size_t>(A_max) * static_cast<size_t>(moe_padded_inner_width(f)) *
-                    static_cast<size_t>(elem_bytes(dt))) +
-           kAlign;
+    if (A_max < 0 || f < 1 || h < 0 || !valid_dtype(dt)) return 0;
+    const int64_t fp = moe_padded_inner_width(f);
+    // H (A_max x fp), then the down-projection's fp32 partial tiles when its K is split
+    return align_up(static_cast<size_t>(A_max) * static_cast<size_t>(fp) * static_cast<size_t>(elem_bytes(dt))) +
+           align_up(moe::down_partial_bytes(A_max, h, fp, dt == MOE_BF16)) + kAlign;
 }
 
 static moe_status ffn_check(const void* x_perm, const int32_t* offsets, int64_t A_max, int32_t E, int64_t h,

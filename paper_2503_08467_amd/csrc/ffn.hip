@@ -49,6 +49,11 @@ struct GroupedGemm {
     const int32_t* scatter;
     const float* scatter_w;
     int64_t c_rows;
+    // Down-projection only: with ksplit > 1 every tile is computed as ksplit parts of K/ksplit
+    // each, part s written in fp32 to partial[s][row][N] (no scale, no scatter); a reduce
+    // kernel sums the parts in order afterwards.
+    int ksplit;
+    float* partial;
 };
 
 // Source row of grouped row p: p itself, or gather[p] clamped into a (entries past the
@@ -511,13 +516,15 @@ void gemm_bf16_lds(GroupedGemm g) {
 
     const int total_m = tile_prefix<BM>(g.offsets, g.E, tstart);
     const LdsTiles tiles{tstart, g.E};
-    const int total = total_m * g.n_tiles;
+    // work item L = tile L / ks, K part L % ks (ks = 1 unless the down-projection is split)
+    const int ks = (!kUp && g.ksplit > 1) ? g.ksplit : 1;
+    const int total = total_m * g.n_tiles * ks;
     const int per = (total + 7) >> 3;
     const int xcd = blockIdx.x & 7, nslot = gridDim.x >> 3;
     const int t_end = min(total, (xcd + 1) * per);
     const int t_first = xcd * per + static_cast<int>(blockIdx.x >> 3);
     if (t_first >= t_end) return;
-    const int nk = g.K / BK;
+    const int nk = g.K / BK / ks;  // K steps per work item
 
     const int tid = threadIdx.x, lane = tid & 63;
     // the wave index is uniform across a wave; say so, so that per-wave choices stay scalar
@@ -549,7 +556,8 @@ void gemm_bf16_lds(GroupedGemm g) {
     int lt = t_first, lk = 0;
     const unsigned char *src_a = nullptr, *src_b0 = nullptr, *src_b1 = nullptr;
     auto set_tile = [&](int L) {
-        const TileGeom t = tile_geom<BM, BN>(g, tiles, total_m, L);
+        const TileGeom t = tile_geom<BM, BN>(g, tiles, total_m, L / ks);
+        const int64_t k0 = static_cast<int64_t>(L % ks) * nk;  // first K block of the work item
         const int64_t rb = kUp ? 2 * static_cast<int64_t>(g.K) : 64;
         if (kUp && g.gather) {
             // this lane's activation rows come from the gathered source rows (the index
@@ -565,9 +573,10 @@ void gemm_bf16_lds(GroupedGemm g) {
             }
             src_a = uniform_ptr(g.a);
         } else {
-            src_a = uniform_ptr(static_cast<const unsigned char*>(g.a) + t.row_base * rb);
+            src_a = uniform_ptr(static_cast<const unsigned char*>(g.a) + t.row_base * rb +
+                                (kUp ? 0 : k0 * g.rows_max * 64));
         }
-        const int64_t boff = (t.e * g.b_estride) * 2 + static_cast<int64_t>(t.n_base) * 64;
+        const int64_t boff = (t.e * g.b_estride) * 2 + static_cast<int64_t>(t.n_base) * 64 + k0 * g.N * 64;
         src_b0 = uniform_ptr(static_cast<const unsigned char*>(g.b) + boff);
         src_b1 = NB > 1 ? uniform_ptr(static_cast<const unsigned char*>(g.b2) + boff) : src_b0;
     };
@@ -625,7 +634,7 @@ void gemm_bf16_lds(GroupedGemm g) {
     constexpr bool kAccInAgpr = S::kPerCU == 1;
     int consumed = 0;
     for (int ct = t_first; ct < t_end; ct += nslot) {
-        const TileGeom t = tile_geom<BM, BN>(g, tiles, total_m, ct);
+        const TileGeom t = tile_geom<BM, BN>(g, tiles, total_m, ct / ks);
         // Row blocks of this wave that hold valid rows.  Valid rows start at the tile's first
         // row unless the tile was shifted back at the end of the buffer; then all count.  The
         // count is rounded up to MI / 2 or MI so that three loop bodies cover every case.
@@ -704,6 +713,32 @@ void gemm_bf16_lds(GroupedGemm g) {
         // 32-column block; its four groups sit 8 elements apart (immediate store offsets).
         typedef typename std::conditional<OB, bf16_t, float>::type OutT;
         const int64_t row_lo = t.row0 > 0 ? t.row0 : 0;
+        if (ks > 1) {
+            // a K part: its fp32 sums go to partial[part][row][N], the reduce kernel finishes
+            float* const part = g.partial + static_cast<int64_t>(ct % ks) * g.rows_max * g.N;
+#pragma unroll
+            for (int i = 0; i < MI; ++i) {
+                if (i >= nv) break;
+                const int64_t row = t.row_base + wm * (BM / 2) + i * 32 + l32;
+                const bool row_ok = row >= row_lo && row < t.row_end;
+#pragma unroll
+                for (int j = 0; j < NI; ++j) {
+                    const int col0 = t.n_base + wn * (BN / WN) + j * 32 + 4 * lhi;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int col = col0 + 8 * q;
+                        if (row_ok && col >= t.n0 && col < g.N)
+                            *reinterpret_cast<float4*>(part + row * g.N + col) =
+                                make_float4(acc_read<kAccInAgpr>(acc[0][i][j][4 * q]),
+                                            acc_read<kAccInAgpr>(acc[0][i][j][4 * q + 1]),
+                                            acc_read<kAccInAgpr>(acc[0][i][j][4 * q + 2]),
+                                            acc_read<kAccInAgpr>(acc[0][i][j][4 * q + 3]));
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                }
+            }
+            continue;
+        }
 #pragma unroll
         for (int i = 0; i < MI; ++i) {
             if (i >= nv) break;  // no valid row in this block or any later one
@@ -1120,6 +1155,56 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GroupedGemm g) {
     }
 }
 
+// ------------------------------------------------------------------ split-K reduce
+//
+// out[p] = sum over s of partial[s][p] (s ascending) for the grouped rows p of the call,
+// [offsets[0], offsets[E]); with scatter (top-1), out[t] = w[t] * that sum for
+// t = scatter[p] instead (the down-projection's own epilogue, applied after the parts
+// meet).  N % 4 == 0.
+
+template <bool OB>
+__global__ __launch_bounds__(256) void split_reduce(const float* __restrict__ partial, int S, int64_t rows_max,
+                                                     int N, const int32_t* __restrict__ offsets, int E,
+                                                     void* __restrict__ out, int ldo,
+                                                     const int32_t* __restrict__ scatter,
+                                                     const float* __restrict__ scatter_w, int64_t c_rows) {
+    const int64_t p0 = offsets[0];
+    const int64_t p1 = offsets[E] < rows_max ? offsets[E] : rows_max;
+    const int nv = N / 4;
+    const int64_t n = (p1 - p0) * nv;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n;
+         i += static_cast<int64_t>(gridDim.x) * 256) {
+        const int64_t p = p0 + i / nv;
+        const int c = static_cast<int>(i % nv) * 4;
+        float4 v = *reinterpret_cast<const float4*>(partial + p * N + c);
+        for (int s = 1; s < S; ++s) {
+            const float4 u = *reinterpret_cast<const float4*>(partial + (static_cast<int64_t>(s) * rows_max + p) * N + c);
+            v.x += u.x;
+            v.y += u.y;
+            v.z += u.z;
+            v.w += u.w;
+        }
+        int64_t row = p;
+        if (scatter) {
+            const int64_t t = scatter[p];
+            row = t < 0 ? 0 : (t >= c_rows ? c_rows - 1 : t);
+            const float w = scatter_w[row];
+            v.x *= w;
+            v.y *= w;
+            v.z *= w;
+            v.w *= w;
+        }
+        if (OB) {
+            uint2 pk;
+            pk.x = pack_bf16x2(v.x, v.y);
+            pk.y = pack_bf16x2(v.z, v.w);
+            *reinterpret_cast<uint2*>(static_cast<bf16_t*>(out) + row * ldo + c) = pk;
+        } else {
+            *reinterpret_cast<float4*>(static_cast<float*>(out) + row * ldo + c) = v;
+        }
+    }
+}
+
 // ------------------------------------------------------------------ launch
 
 int64_t row_tile_bound(int64_t A_max, int E, int bm) {
@@ -1175,7 +1260,7 @@ hipError_t run_bf16_lds(GroupedGemm g, int64_t A_max, hipStream_t s) {
         hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
     if (attr != hipSuccess) return attr;
     g.n_tiles = static_cast<int>(ceil_div(g.N, S::kBN));
-    const int64_t tiles = row_tile_bound(A_max, g.E, BM) * g.n_tiles;
+    const int64_t tiles = row_tile_bound(A_max, g.E, BM) * g.n_tiles * (g.ksplit > 1 ? g.ksplit : 1);
     if (tiles == 0) return hipSuccess;
     // persistent grid: at most per_cu workgroups per CU, a multiple of the 8 XCDs
     const int64_t blocks = round_up(std::min<int64_t>(tiles, static_cast<int64_t>(per_cu) * device_cus()), 8);
@@ -1218,6 +1303,10 @@ template <int EPI, bool OB>
 hipError_t run_bf16_best(GroupedGemm g, int64_t A_max, hipStream_t s) {
     constexpr bool kUp = EPI != kEpiNone;
     if constexpr (kUp) {
+        // Decode-sized calls (at most 128 rows: a few row tiles) take 128-column tiles, twice
+        // as many workgroups streaming the weights (measured: about 10 us less on a 64-token
+        // top-2 step; no gain from 256 rows up, where the tiles already cover the CUs).
+        if (A_max <= 128 && g.K % 32 == 0) return run_bf16_lds<128, 128, 32, 3, EPI, OB>(g, A_max, s);
         // activation rows in 128-byte pieces when K allows it (see gemm_up_pairs)
         if constexpr (OB) {
             if (g.K % 64 == 0) return run_up_pairs<EPI>(g, A_max, s);
@@ -1226,6 +1315,7 @@ hipError_t run_bf16_best(GroupedGemm g, int64_t A_max, hipStream_t s) {
         return run_bf16<EPI, OB, true>(g, A_max, s);
     } else {
         if (g.K % 32 != 0) return hipErrorInvalidValue;  // not reachable through the C ABI (fp % 128 == 0)
+        if (g.ksplit > 1) return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);
         if (g.N >= 384 && row_tile_bound(A_max, g.E, 128) * ceil_div(g.N, 384) <= device_cus())
             return run_bf16_lds<128, 384, 32, 3, EPI, OB, 4>(g, A_max, s);
         return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);
@@ -1281,9 +1371,25 @@ hipError_t ffn_pair(const void* x_perm, const int32_t* offsets, int64_t grid_row
         g2.scatter_w = scatter_w;
         g2.c_rows = a_rows;
     }
-    if (bf16)
+    if (!bf16) return y_bf16 ? run_f32<kEpiNone, true>(g2, grid_rows, s) : run_f32<kEpiNone, false>(g2, grid_rows, s);
+    // the split is chosen from rows_max (the call's row bound), so a per-expert launch of
+    // this call splits like the grouped one
+    g2.ksplit = down_ksplit(rows_max, fp, true);
+    if (g2.ksplit <= 1)
         return y_bf16 ? run_bf16_best<kEpiNone, true>(g2, grid_rows, s) : run_bf16_best<kEpiNone, false>(g2, grid_rows, s);
-    return y_bf16 ? run_f32<kEpiNone, true>(g2, grid_rows, s) : run_f32<kEpiNone, false>(g2, grid_rows, s);
+    // partial tiles after H in the workspace: ksplit x rows_max x h fp32
+    g2.partial = reinterpret_cast<float*>(static_cast<unsigned char*>(hbuf) + round_up(rows_max * fp * 2, 256));
+    err = y_bf16 ? run_bf16_best<kEpiNone, true>(g2, grid_rows, s) : run_bf16_best<kEpiNone, false>(g2, grid_rows, s);
+    if (err != hipSuccess) return err;
+    const int64_t n4 = grid_rows * (h / 4);
+    const int blocks = static_cast<int>(std::min<int64_t>(ceil_div(n4, 256), 8LL * device_cus()));
+    if (y_bf16)
+        hipLaunchKernelGGL(split_reduce<true>, dim3(blocks), dim3(256), 0, s, g2.partial, g2.ksplit, rows_max, h,
+                           offsets, E, y_perm, h, g2.scatter, g2.scatter_w, g2.c_rows);
+    else
+        hipLaunchKernelGGL(split_reduce<false>, dim3(blocks), dim3(256), 0, s, g2.partial, g2.ksplit, rows_max, h,
+                           offsets, E, y_perm, h, g2.scatter, g2.scatter_w, g2.c_rows);
+    return hipGetLastError();
 }
 
 }  // namespace

@@ -11,6 +11,25 @@ namespace moe {
 constexpr int kInnerAlign = 128;  // packed inner width is a multiple of this
 constexpr int kDispatchChunk = 1024;  // assignments per dispatch workgroup
 
+// K parts of the bf16 down-projection.  A call with few rows has few row tiles, each with a
+// long K loop, and leaves most CUs idle; splitting K spreads the weight reads over more
+// workgroups (fp32 partial tiles, summed in a fixed order afterwards).  A function of the
+// call's sizes only (the row bound, not the routing), so every launch path of one call
+// shape rounds the same way.  fp is the packed inner width (a multiple of kInnerAlign).
+inline int down_ksplit(int64_t A_max, int64_t fp, bool bf16) {
+    if (!bf16 || A_max > 512) return 1;  // measured: no gain from 1024 rows up
+    int s = A_max <= 256 ? 8 : 4;
+    const int64_t nk = fp / 32;  // K steps of 32
+    while (s > 1 && (nk % s != 0 || nk / s < 8)) s >>= 1;
+    return s;
+}
+
+// Bytes of fp32 partial tiles that the split down-projection needs past the H buffer.
+inline size_t down_partial_bytes(int64_t A_max, int64_t h, int64_t fp, bool bf16) {
+    const int s = down_ksplit(A_max, fp, bf16);
+    return s > 1 ? static_cast<size_t>(s) * static_cast<size_t>(A_max) * static_cast<size_t>(h) * 4u : 0u;
+}
+
 hipError_t launch_route(const void* x, bool bf16, int64_t T, int h, const void* wg, int E, int k,
                         const float* bias, int64_t bias_stride, int renorm, int32_t* idx, float* w,
                         hipStream_t s);

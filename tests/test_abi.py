@@ -105,6 +105,23 @@ def test_sizes_follow_the_padded_layout(lib):
     assert lib.moe_ffn_workspace_size(1000, 8, 768, 3072, _lib.MOE_ACT_GELU, _lib.MOE_F32) >= 1000 * 3072 * 4
 
 
+def test_ffn_workspace_holds_split_partials(lib):
+    """Small bf16 calls split the second product's K: fp32 partials of S x A_max x h follow H."""
+    al = lambda v: (v + 255) // 256 * 256
+    ws = lambda A, h, f, dt=_lib.MOE_BF16: lib.moe_ffn_workspace_size(A, 64, h, f, _lib.MOE_ACT_GELU, dt)
+    # decode-sized: 128 rows, fp = 4096 (128 K steps of 32) -> 8 parts
+    assert ws(128, 1024, 4096) == al(128 * 4096 * 2) + al(8 * 128 * 1024 * 4) + 256
+    assert ws(256, 1024, 4096) == al(256 * 4096 * 2) + al(8 * 256 * 1024 * 4) + 256
+    assert ws(512, 768, 3072) == al(512 * 3072 * 2) + al(4 * 512 * 768 * 4) + 256
+    # fp = 1792: 56 K steps, 8 parts would leave 7 per part -> 4 parts
+    assert ws(128, 4096, 1792) == al(128 * 1792 * 2) + al(4 * 128 * 4096 * 4) + 256
+    # short K: fp = 128 has 4 steps, too few to split
+    assert ws(128, 1024, 128) == al(128 * 128 * 2) + 256
+    # large calls and fp32 never split
+    assert ws(513, 768, 3072) == al(513 * 3072 * 2) + 256
+    assert ws(128, 1024, 4096, _lib.MOE_F32) == al(128 * 4096 * 4) + 256
+
+
 def test_ffn_and_combine_reject_bad_arguments(lib):
     ws = lib.moe_ffn_workspace_size(64, 8, 64, 32, _lib.MOE_ACT_GELU, _lib.MOE_BF16)
     ok_args = [A16, A16, 64, 8, 64, 32, _lib.MOE_ACT_GELU, _lib.MOE_BF16, A16, A16, _lib.MOE_BF16, A16, ws, None]
@@ -156,8 +173,10 @@ def test_bench_names_the_expert_step_kernels():
           "void moe::(anonymous namespace)::gemm_f32<0, false>(moe::(anonymous namespace)::GroupedGemm)"]
     down = ["void moe::(anonymous namespace)::gemm_bf16_lds<128, 384, 32, 3, 3, true, 4>(moe::(anonymous namespace)::GroupedGemm)",
             "void moe::(anonymous namespace)::gemm_bf16_lds<128, 256, 32, 3, 3, false, 2>(moe::(anonymous namespace)::GroupedGemm)",
-            "void moe::(anonymous namespace)::gemm_f32<3, true>(moe::(anonymous namespace)::GroupedGemm)"]
+            "void moe::(anonymous namespace)::gemm_f32<3, true>(moe::(anonymous namespace)::GroupedGemm)",
+            "void moe::(anonymous namespace)::split_reduce<true>(float const*, int, long, int, int const*, int, "
+            "void*, int, int const*, float const*, long)"]
     assert all(bench.is_ffn_kernel(n) for n in up + down)
     assert not bench.is_ffn_kernel("void moe::(anonymous namespace)::route_lds_kernel<1>(unsigned short const*)")
     assert [bench.ffn_matrix(n) for n in up] == ["up"] * 3
-    assert [bench.ffn_matrix(n) for n in down] == ["down"] * 3
+    assert [bench.ffn_matrix(n) for n in down] == ["down"] * 4

@@ -186,6 +186,9 @@ def _run_ffn(x, w1, w3, w2, offsets, act, dtype, out_dtype=None, col0=0, f=None)
     ([513, 40, 0, 255], 768, 512),
     ([700, 333], 256, 200),                    # >= 512 rows per expert: 256-row tiles, ragged
     ([1100, 0, 1500, 3], 512, 384),
+    ([60, 0, 50, 9], 128, 1000),               # <= 128 rows: 128-column up tiles, K of the down in 4 parts
+    ([100, 7, 0, 120], 192, 2048),             # <= 256 rows: down K in 8 parts
+    ([200, 0, 61, 3], 256, 2048),              # <= 512 rows: down K in 4 parts
 ])
 def test_ffn_parity(dtype, act, counts, h, f):
     rng = np.random.default_rng(sum(counts) + h + f)
@@ -201,6 +204,7 @@ def test_ffn_parity(dtype, act, counts, h, f):
     ([300, 0, 5, 129, 128, 1], 256, 200),
     ([0, 0, 77], 72, 128),
     ([700, 333, 0], 256, 200),
+    ([60, 0, 50, 9], 128, 1000),  # split down-projection K: both paths split alike
 ])
 def test_per_expert_launches_match_grouped(dtype, act, counts, h, f):
     """The per-expert-launch ablation computes the same tiles as the grouped launch: equal
@@ -221,7 +225,8 @@ def test_per_expert_launches_match_grouped(dtype, act, counts, h, f):
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("act", ["gelu", "swiglu"])
-@pytest.mark.parametrize("T,k,E,h,f", [(700, 2, 6, 256, 200), (90, 1, 3, 72, 128), (1500, 1, 4, 768, 384)])
+@pytest.mark.parametrize("T,k,E,h,f", [(700, 2, 6, 256, 200), (90, 1, 3, 72, 128), (1500, 1, 4, 768, 384),
+                                        (50, 2, 5, 128, 1024)])
 def test_gathered_rows_match_x_perm(dtype, act, T, k, E, h, f):
     """The expert step reading x[row_src[p]] itself equals the one reading x_perm, bit for
     bit; some ids are invalid (dropped), so row_src has unwritten entries past offsets[E]."""
@@ -256,7 +261,8 @@ def test_gathered_rows_match_x_perm(dtype, act, T, k, E, h, f):
 
 @pytest.mark.parametrize("dtype,out_dtype", [("bf16", "bf16"), ("bf16", "f32"), ("f32", "f32")])
 @pytest.mark.parametrize("act", ["gelu", "swiglu"])
-@pytest.mark.parametrize("T,E,h,f", [(700, 6, 256, 200), (90, 3, 72, 128), (1300, 5, 768, 384)])
+@pytest.mark.parametrize("T,E,h,f", [(700, 6, 256, 200), (90, 3, 72, 128), (1300, 5, 768, 384),
+                                     (100, 3, 128, 1024)])  # split down K: weighted sum in the reduce
 def test_top1_step_writes_weighted_rows(dtype, out_dtype, act, T, E, h, f):
     """moe_expert_ffn_shard_top1 = the expert step plus the top-1 combine: y[t] = w[t] *
     FFN_e(x[t]).  Tokens whose only pick is invalid are dropped and left unwritten."""
