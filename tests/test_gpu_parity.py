@@ -49,7 +49,7 @@ def _check_route(x, wg, bias, k, renorm, dtype, exact_products):
 
 
 @pytest.mark.parametrize("name,T", [("c1", 512), ("c2", 8192), ("c3", 16384), ("c4", 4096), ("c5", 32768),
-                                    ("c5dec", 64)])
+                                    ("c5dec", 64), ("paper128", 30000)])
 def test_route_parity_on_workloads(name, T):
     L = synth.make(name, seed=0, weights=False, T=T)
     gi, unsure = _check_route(L.x, L.wg, L.sel_bias, L.cfg.k, L.cfg.renorm, L.cfg.dtype, L.cfg.dtype == "bf16")
@@ -60,7 +60,8 @@ def test_route_parity_on_workloads(name, T):
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("T,h,E,k", [(1, 8, 1, 1), (17, 72, 3, 2), (100, 256, 16, 16), (65, 136, 17, 4),
-                                     (130, 64, 64, 2), (33, 512, 200, 8), (64, 96, 256, 3), (257, 1024, 128, 1)])
+                                     (130, 64, 64, 2), (33, 512, 200, 8), (64, 96, 256, 3), (257, 1024, 128, 1),
+                                     (16449, 64, 136, 2)])  # more 64-token workgroups than CUs
 @pytest.mark.parametrize("bias_kind", ["none", "row", "shared"])
 def test_route_shapes_and_bias(dtype, T, h, E, k, bias_kind):
     rng = np.random.default_rng(T * 1000 + E)
