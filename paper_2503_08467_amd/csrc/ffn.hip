@@ -5,17 +5,21 @@
 //   GEMM1   H[p, n] = act(x_perm[p] . W1^T[e][n])       (SwiGLU: silu(.W1) * (.W3))
 //   GEMM2   y_perm[p, c] = H[p] . W2^T[e][c]
 //
-// Each workgroup first turns offsets[] into a per-expert prefix of row tiles (in LDS),
-// then maps its linear tile id to (expert, row tile, column tile).  Tiles past the last
-// real one exit at once, so the grid can be sized from the host-known bound A_max
-// without reading the counts back.
+// Each workgroup first turns offsets[] into a per-expert prefix of row tiles, then maps
+// linear tile ids to (expert, row tile, column tile).  The grid is persistent (sized from
+// the host-known bound A_max, at most two workgroups per CU, a multiple of the 8 XCDs), so
+// the counts are never read back to the host.
 //
-// bf16 path: 128-row tiles, 4 waves in a 2 x 2 arrangement, v_mfma_f32_32x32x16_bf16
-// with fp32 accumulation, K staged through double-buffered LDS in steps of 64 with the
-// next step's global loads in flight during the current step's MFMAs.  The epilogue
-// applies the activation in fp32, rounds once, and goes through LDS so that every global
-// store is a full 16-byte row segment.
-// fp32 path: the same scheduling over a plain LDS-tiled fp32 FMA kernel (64 x 64 tiles).
+// bf16 path (gemm_bf16_lds, gemm_up_pairs): 128-row tiles, 256 (or 384 / 128) weight rows
+// per tile, v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  Weights and H are stored
+// K-blocked (blocks of 32 K values, all rows side by side), so every stage of 32 K values
+// of a run of rows is one contiguous stretch that 1 KiB direct-to-LDS loads fetch; three
+// LDS stages, two in flight across K steps and tiles.  The epilogue applies the activation
+// in fp32, rounds once, and stores 8-byte vectors straight from the accumulators (into
+// K-blocked H for GEMM1).  Calls of at most 512 rows split GEMM2's K into parts summed by
+// split_reduce in a fixed order.
+// fp32 path (gemm_f32): 64 x 64 tiles on v_mfma_f32_32x32x2_f32, row-major operands staged
+// through two LDS buffers from registers.
 #include "common.h"
 #include "kernels.h"
 #include "lds_dma.h"
@@ -363,6 +367,29 @@ struct LdsShape {
     static_assert(BK == 32, "the K-blocked operands come in blocks of 32");
 };
 
+// Stores one lane's share of a 32 x 32 bf16 output block.  The MFMA layout leaves lane
+// (row, half) with columns 8 q + 4 half .. 8 q + 4 half + 3 of its row, q = 0..3, packed
+// as pk[q].  Lanes l and l ^ 32 hold the same row; they swap two of their four groups, so
+// that each then holds two runs of 8 consecutive columns, 8 half .. 8 half + 7 and 16 +
+// 8 half .. 16 + 8 half + 7, stored as one 16-byte vector each: half the store
+// instructions of 8-byte groups, and 32 contiguous bytes of every row per instruction.
+// dst = the lane's row at column 8 half of the block (the second run is dst + 16); ok0 /
+// ok1 say whether each run is stored.  Every lane of the wave must call it (the swap).
+__device__ __forceinline__ void store_block_bf16(bf16_t* dst, const uint2 (&pk)[4], int lhi, bool ok0, bool ok1) {
+    const uint2 ga = lhi ? pk[0] : pk[1], gb = lhi ? pk[2] : pk[3];
+    uint2 ra, rb;
+    ra.x = __shfl_xor(ga.x, 32, kWave);
+    ra.y = __shfl_xor(ga.y, 32, kWave);
+    rb.x = __shfl_xor(gb.x, 32, kWave);
+    rb.y = __shfl_xor(gb.y, 32, kWave);
+    if (ok0)
+        *reinterpret_cast<uint4*>(dst) =
+            lhi ? make_uint4(ra.x, ra.y, pk[1].x, pk[1].y) : make_uint4(pk[0].x, pk[0].y, ra.x, ra.y);
+    if (ok1)
+        *reinterpret_cast<uint4*>(dst + 16) =
+            lhi ? make_uint4(rb.x, rb.y, pk[3].x, pk[3].y) : make_uint4(pk[2].x, pk[2].y, rb.x, rb.y);
+}
+
 // One accumulator value for the epilogue.  With 256 accumulator registers per lane they
 // live in AGPRs, and VALU work needs them in VGPRs; left to itself the compiler copies all of
 // them at once when the K loop ends, which needs every VGPR and spills the loop's live
@@ -709,9 +736,9 @@ void gemm_bf16_lds(GroupedGemm g) {
 
         // ---- epilogue of tile ct.  D[n][m] layout: lane holds activation row l32 of the
         // block; register r holds weight row 8 * (r / 4) + 4 * lhi + r % 4, i.e. 4
-        // consecutive output columns per group r / 4.  The lane's address is formed once per
-        // 32-column block; its four groups sit 8 elements apart (immediate store offsets).
-        typedef typename std::conditional<OB, bf16_t, float>::type OutT;
+        // consecutive output columns per group r / 4.  bf16 output: two 16-byte runs per
+        // lane and block (store_block_bf16); fp32 output: the four groups as 16-byte vectors,
+        // 8 elements apart from the lane's address (immediate store offsets).
         const int64_t row_lo = t.row0 > 0 ? t.row0 : 0;
         if (ks > 1) {
             // a K part: its fp32 sums go to partial[part][row][N], the reduce kernel finishes
@@ -753,34 +780,48 @@ void gemm_bf16_lds(GroupedGemm g) {
             }
 #pragma unroll
             for (int j = 0; j < NI; ++j) {
-                // this lane's first column in the block; the 4-column groups col .. col + 3
-                // never cross a 32-column block (K-blocked H) nor the end of a row (N % 4 == 0)
-                const int col0 = t.n_base + wn * (BN / WN) + j * 32 + 4 * lhi;
-                OutT* const dst = static_cast<OutT*>(g.c) +
-                                  (kUp ? ((static_cast<int64_t>(col0) >> 5) * g.rows_max + row) * 32 + (col0 & 31)
-                                       : row * g.ldc + col0);
+                const int cb = t.n_base + wn * (BN / WN) + j * 32;  // the block's first column
+                if constexpr (OB) {
+                    uint2 pk[4];
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int col = col0 + 8 * q;
-                    float v[4];
+                    for (int q = 0; q < 4; ++q) {
+                        float v[4];
 #pragma unroll
-                    for (int c = 0; c < 4; ++c)
-                        v[c] = scale * epilogue_fast<EPI>(acc_read<kAccInAgpr>(acc[0][i][j][4 * q + c]),
-                                                          acc_read<kAccInAgpr>(acc[NB - 1][i][j][4 * q + c]));
-                    if (row_ok && col >= t.n0 && col < g.N) {
-                        if (OB) {
-                            uint2 pk;
-                            pk.x = pack_bf16x2(v[0], v[1]);
-                            pk.y = pack_bf16x2(v[2], v[3]);
-                            *reinterpret_cast<uint2*>(dst + 8 * q) = pk;
-                        } else {
-                            *reinterpret_cast<float4*>(dst + 8 * q) = make_float4(v[0], v[1], v[2], v[3]);
-                        }
+                        for (int c = 0; c < 4; ++c)
+                            v[c] = scale * epilogue_fast<EPI>(acc_read<kAccInAgpr>(acc[0][i][j][4 * q + c]),
+                                                              acc_read<kAccInAgpr>(acc[NB - 1][i][j][4 * q + c]));
+                        pk[q].x = pack_bf16x2(v[0], v[1]);
+                        pk[q].y = pack_bf16x2(v[2], v[3]);
                     }
-                    // one group at a time: keeps the scheduler from pulling every accumulator
-                    // into VGPRs at once
-                    __builtin_amdgcn_sched_barrier(0);
+                    // runs of 8 columns from c0 and c0 + 16: inside one 32-column block of
+                    // K-blocked H (N, n0 and cb are multiples of 32 there), or inside a row of
+                    // y (N, n0 and cb are multiples of 8), wholly before n0 or wholly after it
+                    const int c0 = cb + 8 * lhi;
+                    bf16_t* const dst = static_cast<bf16_t*>(g.c) +
+                                        (kUp ? ((static_cast<int64_t>(cb) >> 5) * g.rows_max + row) * 32 + 8 * lhi
+                                             : row * g.ldc + c0);
+                    store_block_bf16(dst, pk, lhi, row_ok && c0 >= t.n0 && c0 < g.N,
+                                     row_ok && c0 + 16 >= t.n0 && c0 + 16 < g.N);
+                } else {
+                    // fp32 y_perm (down-projection): groups of 4 columns, N % 4 == 0
+                    const int col0 = cb + 4 * lhi;
+                    float* const dst = static_cast<float*>(g.c) + row * g.ldc + col0;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int col = col0 + 8 * q;
+                        float v[4];
+#pragma unroll
+                        for (int c = 0; c < 4; ++c)
+                            v[c] = scale * epilogue_fast<EPI>(acc_read<kAccInAgpr>(acc[0][i][j][4 * q + c]),
+                                                              acc_read<kAccInAgpr>(acc[NB - 1][i][j][4 * q + c]));
+                        if (row_ok && col >= t.n0 && col < g.N)
+                            *reinterpret_cast<float4*>(dst + 8 * q) = make_float4(v[0], v[1], v[2], v[3]);
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
                 }
+                // one block at a time: keeps the scheduler from pulling every accumulator
+                // into VGPRs at once
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
     }
@@ -994,24 +1035,22 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_up_pairs(GroupedGemm g) {
             const bool row_ok = row >= row_lo && row < t.row_end;
 #pragma unroll
             for (int j = 0; j < NI; ++j) {
-                const int col0 = t.n_base + wn * (BN / 2) + j * 32 + 4 * lhi;
-                bf16_t* const dst = static_cast<bf16_t*>(g.c) +
-                                    ((static_cast<int64_t>(col0) >> 5) * g.rows_max + row) * 32 + (col0 & 31);
+                const int cb = t.n_base + wn * (BN / 2) + j * 32;  // the block's first column
+                uint2 pk[4];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int col = col0 + 8 * q;
                     float v[4];
 #pragma unroll
                     for (int c = 0; c < 4; ++c)
                         v[c] = epilogue_fast<EPI>(acc[0][i][j][4 * q + c], acc[NB - 1][i][j][4 * q + c]);
-                    if (row_ok && col >= t.n0 && col < g.N) {
-                        uint2 pk;
-                        pk.x = pack_bf16x2(v[0], v[1]);
-                        pk.y = pack_bf16x2(v[2], v[3]);
-                        *reinterpret_cast<uint2*>(dst + 8 * q) = pk;
-                    }
-                    __builtin_amdgcn_sched_barrier(0);
+                    pk[q].x = pack_bf16x2(v[0], v[1]);
+                    pk[q].y = pack_bf16x2(v[2], v[3]);
                 }
+                bf16_t* const dst = static_cast<bf16_t*>(g.c) +
+                                    ((static_cast<int64_t>(cb) >> 5) * g.rows_max + row) * 32 + 8 * lhi;
+                const bool ok = row_ok && cb >= t.n0 && cb < g.N;  // N, n0, cb: multiples of 32
+                store_block_bf16(dst, pk, lhi, ok, ok);
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
     }
