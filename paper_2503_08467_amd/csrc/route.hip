@@ -56,121 +56,6 @@ struct GateFrag<float> {
 };
 
 constexpr int kWaves = 4;
-constexpr int kNone = 0x7fffffff;  // no expert picked (yet)
-
-// Lane moves inside each aligned group of 8 lanes: xor 1 and xor 2 within each quad
-// (quad_perm), then the mirror within each half row, which pairs every lane with one of the
-// other quad.  Applied in turn they combine all 8 lanes of a commutative, associative
-// reduction (max, sum in a fixed tree, the arg-max order below), leaving every lane with the
-// same result, in register-to-register moves instead of LDS-routed shuffles.
-constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141;
-
-template <int CTRL>
-__device__ __forceinline__ int dpp_i(int v) {
-    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xf, 0xf, false);
-}
-template <int CTRL>
-__device__ __forceinline__ float dpp_f(float v) {
-    return __int_as_float(dpp_i<CTRL>(__float_as_int(v)));
-}
-
-// One step of the group arg-max: the higher score wins, equal scores go to the lower id.
-template <int CTRL>
-__device__ __forceinline__ void argmax_step(float& bs, float& bl, int& be) {
-    const float os = dpp_f<CTRL>(bs), ol = dpp_f<CTRL>(bl);
-    const int oe = dpp_i<CTRL>(be);
-    if (oe != kNone && (be == kNone || os > bs || (os == bs && oe < be))) {
-        bs = os;
-        bl = ol;
-        be = oe;
-    }
-}
-
-// Softmax weights and top-k picks of one token whose logits are spread over the 8 lanes of
-// its group: slot j of lane q holds expert q + 8 j (STRIDED) or NV q + j.  lv = logit (-inf
-// past E), sv = selection score (logit + bias, -inf past E).  The softmax runs over the
-// logits, the picks over the scores: k rounds of arg-max over the experts not yet taken,
-// each pick weighted by its softmax probability (renormalised over the k picks if asked).
-// Ties: each lane scans its slots upward with a strict comparison and the group reduction
-// prefers the lower id, so equal scores go to the lower expert id.
-// If `store`, the token's ids and weights go to idx_t[0..k) and w_t[0..k).
-template <int NV, bool STRIDED>
-__device__ __forceinline__ void route_select(const float (&lv)[NV], const float (&sv)[NV], int q, int E, int k,
-                                             int renorm, bool store, int32_t* idx_t, float* w_t) {
-    auto expert = [&](int j) { return STRIDED ? q + 8 * j : NV * q + j; };
-    float mx = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < NV; ++j) mx = fmaxf(mx, lv[j]);
-    mx = fmaxf(mx, dpp_f<kDppXor1>(mx));
-    mx = fmaxf(mx, dpp_f<kDppXor2>(mx));
-    mx = fmaxf(mx, dpp_f<kDppHalfMirror>(mx));
-    float den = 0.f;
-#pragma unroll
-    for (int j = 0; j < NV; ++j) den += expert(j) < E ? expf(lv[j] - mx) : 0.f;
-    den += dpp_f<kDppXor1>(den);
-    den += dpp_f<kDppXor2>(den);
-    den += dpp_f<kDppHalfMirror>(den);
-
-    uint32_t taken = 0;
-    auto pick = [&](float& p, int& id) {
-        float bs = -INFINITY, bl = -INFINITY;
-        int be = kNone;
-#pragma unroll
-        for (int j = 0; j < NV; ++j) {
-            const int e = expert(j);
-            if (e < E && !((taken >> j) & 1u) && (sv[j] > bs || be == kNone)) {
-                bs = sv[j];
-                bl = lv[j];
-                be = e;
-            }
-        }
-        argmax_step<kDppXor1>(bs, bl, be);
-        argmax_step<kDppXor2>(bs, bl, be);
-        argmax_step<kDppHalfMirror>(bs, bl, be);
-        const bool found = be != kNone;
-        if (found) {
-            const int owner = STRIDED ? (be & 7) : be / NV, slot = STRIDED ? (be >> 3) : be - NV * q;
-            if (owner == q) taken |= 1u << slot;
-        }
-        p = found ? expf(bl - mx) / den : 0.f;
-        id = found ? be : -1;
-    };
-    float wsum = 0.f;
-    if (k <= 8) {
-        // picks kept in registers; the weights are written once, already renormalised
-        float pj[8];
-        int ej[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            if (j < k) {
-                pick(pj[j], ej[j]);
-                wsum += pj[j];
-            }
-        }
-        if (store) {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                if (j < k) {
-                    idx_t[j] = ej[j];
-                    w_t[j] = renorm ? pj[j] / wsum : pj[j];
-                }
-            }
-        }
-        return;
-    }
-    for (int j = 0; j < k; ++j) {
-        float p;
-        int id;
-        pick(p, id);
-        wsum += p;
-        if (store) {
-            idx_t[j] = id;
-            w_t[j] = p;
-        }
-    }
-    if (renorm && store)
-        for (int j = 0; j < k; ++j) w_t[j] = w_t[j] / wsum;
-}
 
 template <int NB>
 constexpr int route_ldw() { return NB * 32 + 8; }  // padded row: 8 token rows hit 8 bank groups
@@ -226,6 +111,7 @@ __global__ __launch_bounds__(kWaves * kWave) void route_kernel(const Tin* __rest
     const int tt = wave * 8 + (lane >> 3), q = lane & 7;
     const int64_t t = tok0 + tt;
     float lv[NV], sv[NV];
+    float mx = -INFINITY;
 #pragma unroll
     for (int j = 0; j < NV; ++j) {
         const int e = q + 8 * j;
@@ -234,8 +120,52 @@ __global__ __launch_bounds__(kWaves * kWave) void route_kernel(const Tin* __rest
         const bool ok = e < E;
         lv[j] = ok ? v : -INFINITY;
         sv[j] = ok ? ((bias && t < T) ? v + bias[t * bias_stride + e] : v) : -INFINITY;
+        mx = fmaxf(mx, lv[j]);
     }
-    route_select<NV, true>(lv, sv, q, E, k, renorm, q == 0 && t < T, idx + t * k, w + t * k);
+#pragma unroll
+    for (int o = 1; o < 8; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+    float den = 0.f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) den += (q + 8 * j < E) ? expf(lv[j] - mx) : 0.f;
+#pragma unroll
+    for (int o = 1; o < 8; o <<= 1) den += __shfl_xor(den, o, kWave);
+
+    uint32_t taken = 0;
+    float wsum = 0.f;
+    for (int j = 0; j < k; ++j) {
+        float bs = -INFINITY, bl = -INFINITY;
+        int be = 0x7fffffff;
+#pragma unroll
+        for (int jj = 0; jj < NV; ++jj) {
+            const int e = q + 8 * jj;
+            if (e < E && !((taken >> jj) & 1u) && (sv[jj] > bs || be == 0x7fffffff)) {
+                bs = sv[jj];
+                bl = lv[jj];
+                be = e;
+            }
+        }
+#pragma unroll
+        for (int o = 1; o < 8; o <<= 1) {
+            const float os = __shfl_xor(bs, o, kWave);
+            const float ol = __shfl_xor(bl, o, kWave);
+            const int oe = __shfl_xor(be, o, kWave);
+            if (oe != 0x7fffffff && (be == 0x7fffffff || os > bs || (os == bs && oe < be))) {
+                bs = os;
+                bl = ol;
+                be = oe;
+            }
+        }
+        const bool found = be != 0x7fffffff;
+        if (found && (be & 7) == q) taken |= 1u << (be >> 3);
+        const float p = found ? expf(bl - mx) / den : 0.f;
+        wsum += p;
+        if (q == 0 && t < T) {
+            idx[t * k + j] = found ? be : -1;
+            w[t * k + j] = p;
+        }
+    }
+    if (renorm && q == 0 && t < T)
+        for (int j = 0; j < k; ++j) w[t * k + j] = w[t * k + j] / wsum;
 }
 
 // ---------------------------------------------------------------- bf16, h % 64 == 0, E > 32
@@ -388,6 +318,7 @@ __global__ __launch_bounds__(kWaves * kWave) void route_lds_kernel(const bf16_t*
         const int tt = pass * 32 + wave * 8 + (lane >> 3);
         const int64_t t = tok0 + tt;
         float lv[NV], sv[NV];
+        float mx = -INFINITY;
 #pragma unroll
         for (int j = 0; j < NV; ++j) {
             const int e = NV * q + j;
@@ -395,8 +326,55 @@ __global__ __launch_bounds__(kWaves * kWave) void route_lds_kernel(const bf16_t*
             const bool ok = e < E;
             lv[j] = ok ? v : -INFINITY;
             sv[j] = ok ? v + bv[pass][j] : -INFINITY;
+            mx = fmaxf(mx, lv[j]);
         }
-        route_select<NV, false>(lv, sv, q, E, k, renorm, q == 0 && t < T, idx + t * k, w + t * k);
+#pragma unroll
+        for (int o = 1; o < 8; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+        float den = 0.f;
+#pragma unroll
+        for (int j = 0; j < NV; ++j) den += (NV * q + j < E) ? expf(lv[j] - mx) : 0.f;
+#pragma unroll
+        for (int o = 1; o < 8; o <<= 1) den += __shfl_xor(den, o, kWave);
+
+        // k rounds of arg-max over the selection score; equal scores -> lower expert id
+        // (each lane scans its experts upward with a strict comparison, and the lane
+        // reduction prefers the lower id on ties)
+        uint32_t taken = 0;
+        float wsum = 0.f;
+        for (int j = 0; j < k; ++j) {
+            float bs = -INFINITY, bl = -INFINITY;
+            int be = 0x7fffffff;
+#pragma unroll
+            for (int jj = 0; jj < NV; ++jj) {
+                const int e = NV * q + jj;
+                if (e < E && !((taken >> jj) & 1u) && (sv[jj] > bs || be == 0x7fffffff)) {
+                    bs = sv[jj];
+                    bl = lv[jj];
+                    be = e;
+                }
+            }
+#pragma unroll
+            for (int o = 1; o < 8; o <<= 1) {
+                const float os = __shfl_xor(bs, o, kWave);
+                const float ol = __shfl_xor(bl, o, kWave);
+                const int oe = __shfl_xor(be, o, kWave);
+                if (oe != 0x7fffffff && (be == 0x7fffffff || os > bs || (os == bs && oe < be))) {
+                    bs = os;
+                    bl = ol;
+                    be = oe;
+                }
+            }
+            const bool found = be != 0x7fffffff;
+            if (found && be / NV == q) taken |= 1u << (be - NV * q);
+            const float p = found ? expf(bl - mx) / den : 0.f;
+            wsum += p;
+            if (q == 0 && t < T) {
+                idx[t * k + j] = found ? be : -1;
+                w[t * k + j] = p;
+            }
+        }
+        if (renorm && q == 0 && t < T)
+            for (int j = 0; j < k; ++j) w[t * k + j] = w[t * k + j] / wsum;
     }
 }
 
