@@ -130,8 +130,10 @@ moe_status moe_pack_weights(const void *w1, const void *w3, const void *w2, int3
                             hipStream_t stream);
 
 /* Bytes of workspace moe_expert_ffn_shard needs: the activated inner rows (A_max x fp) and,
- * for bf16 calls with A_max <= 512, fp32 partial sums of the second product (its K is
- * then split into up to 8 parts so that few rows still occupy the whole GPU). */
+ * for bf16, room for fp32 partial sums of the second product (at most 2048 x h floats):
+ * calls with A_max <= 512 split its K into up to 8 parts so that few rows still occupy
+ * the whole GPU.  Non-decreasing in A_max, so a workspace sized for a bound serves every
+ * call with a smaller A_max. */
 size_t moe_ffn_workspace_size(int64_t A_max, int32_t E, int64_t h, int64_t f, moe_act act,
                               moe_dtype dt);
 

@@ -24,10 +24,18 @@ inline int down_ksplit(int64_t A_max, int64_t fp, bool bf16) {
     return s;
 }
 
-// Bytes of fp32 partial tiles that the split down-projection needs past the H buffer.
+// Bytes of fp32 partial tiles to reserve past the H buffer for a call bound of A_max rows:
+// the most that any call with at most A_max rows needs (down_ksplit * rows * h * 4), so
+// that a workspace sized for a bound also serves every smaller call.  The product is
+// largest at the ends of the two split ranges (256 and 512 rows).
 inline size_t down_partial_bytes(int64_t A_max, int64_t h, int64_t fp, bool bf16) {
-    const int s = down_ksplit(A_max, fp, bf16);
-    return s > 1 ? static_cast<size_t>(s) * static_cast<size_t>(A_max) * static_cast<size_t>(h) * 4u : 0u;
+    int64_t most = 0;
+    for (int64_t end : {int64_t(256), int64_t(512)}) {
+        const int64_t a = A_max < end ? A_max : end;
+        const int64_t s = down_ksplit(a, fp, bf16);
+        if (s > 1 && s * a > most) most = s * a;
+    }
+    return static_cast<size_t>(most) * static_cast<size_t>(h) * 4u;
 }
 
 hipError_t launch_route(const void* x, bool bf16, int64_t T, int h, const void* wg, int E, int k,

@@ -117,9 +117,13 @@ def test_ffn_workspace_holds_split_partials(lib):
     assert ws(128, 4096, 1792) == al(128 * 1792 * 2) + al(4 * 128 * 4096 * 4) + 256
     # short K: fp = 128 has 4 steps, too few to split
     assert ws(128, 1024, 128) == al(128 * 128 * 2) + 256
-    # large calls and fp32 never split
-    assert ws(513, 768, 3072) == al(513 * 3072 * 2) + 256
+    # larger calls do not split but keep the room (a workspace sized for a bound serves
+    # every smaller call); fp32 never splits
+    assert ws(513, 768, 3072) == al(513 * 3072 * 2) + al(2048 * 768 * 4) + 256
     assert ws(128, 1024, 4096, _lib.MOE_F32) == al(128 * 4096 * 4) + 256
+    for h, f in [(1024, 4096), (4096, 1792), (768, 3072), (64, 128), (72, 1000)]:
+        sizes = [ws(a, h, f) for a in range(0, 1100, 7)]
+        assert sizes == sorted(sizes), (h, f)
 
 
 def test_ffn_and_combine_reject_bad_arguments(lib):

@@ -428,6 +428,33 @@ def test_layer_is_deterministic():
     assert torch.equal(y1, y2)
 
 
+def test_layer_call_smaller_than_its_capacity():
+    """A layer sized for 600 tokens, called with 256 (512 assignments, so the second product
+    splits its K): the workspace sized for the larger bound holds the split's partials."""
+    L = synth.make("c5dec", seed=0, T=256)
+    cfg = L.cfg
+    dt = torch.bfloat16
+    packed = moe.pack_weights(to_dev(L.w1, dt), to_dev(L.w2, dt), act=cfg.act)
+    layer = moe.MoEShardLayer(to_dev(L.wg, dt), packed, cfg.k, bool(cfg.renorm), max_tokens=600)
+    y = layer(to_dev(L.x, dt), to_dev(L.sel_bias, torch.float32))
+    torch.cuda.synchronize()
+    ref = oracle.forward(L)
+    same_set, _ = compare_routing(layer.last["idx"].cpu().numpy(), layer.last["w"].cpu().numpy(), ref["idx"],
+                                  ref["w"], L.x, L.wg, L.sel_bias, ref["logits"], cfg.k, True)
+    assert same_set.sum() > 0.9 * cfg.T
+    assert rowwise(np_of(y)[same_set], ref["y"][same_set]) <= TOL["bf16"]
+
+
+def test_layer_is_deterministic_with_split_k():
+    """Decode-sized layer (split second product): two calls give the same bits."""
+    L = synth.make("c5dec", seed=1)
+    layer, x, bias, y1 = _gpu_layer(L)
+    y1 = y1.clone()
+    y2 = layer(x, bias)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+
+
 def test_layer_with_no_tokens():
     L = synth.make("c2", seed=0, T=8, E=8)
     dt = torch.bfloat16
