@@ -74,6 +74,23 @@ def is_ffn_kernel(name: str) -> bool:
     return any(k in name for k in ("gemm_bf16", "gemm_up_pairs", "gemm_f32", "split_reduce"))
 
 
+def is_layer_kernel(name: str) -> bool:
+    """Kernels of a layer step (route, dispatch, expert step, combine), not weight packing,
+    uploads or the copy probe."""
+    return is_ffn_kernel(name) or any(k in name for k in ("route", "dispatch_", "combine_kernel"))
+
+
+def stage_bytes(cfg, fused_gather: bool, top1_fused: bool, bias_per_row: bool) -> dict:
+    """Algorithmic HBM bytes of route, dispatch and combine for one layer call: each input
+    read once and each output written once."""
+    T, k, E, h, A = cfg.T, cfg.k, cfg.E, cfg.h, cfg.A
+    es = 2 if cfg.dtype == "bf16" else 4
+    route = T * h * es + E * h * es + (T * E * 4 if bias_per_row else E * 4) + T * k * 8
+    dispatch = 3 * A * 4 + (2 * E + 1) * 4 + (0 if fused_gather else 2 * A * h * es)
+    combine = 0 if top1_fused else A * h * es + T * h * es + T * k * 8
+    return {"route": route, "dispatch": dispatch, "combine": combine}
+
+
 def ffn_matrix(name: str) -> str:
     """"down" for the down-projection launches (epilogue template argument 3, no activation;
     the sum of its K parts), else "up"."""
@@ -101,13 +118,14 @@ def summarize_counters(config: str, fetch_dir: str, write_dir: str, probe_mib: i
                 per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]) * 1024.0)
         probe = [v for k, vs in per.items() if "neg" in k for v in vs]
         gemm = {k: float(np.mean(v)) for k, v in per.items() if is_ffn_kernel(k)}
+        other = {k: float(np.mean(v)) for k, v in per.items() if is_layer_kernel(k) and not is_ffn_kernel(k)}
         if not probe or not gemm:
             raise SystemExit(f"{d}: missing copy probe or expert-FFN launches for {counter}")
         factor = known / float(np.median(probe))
-        return factor, {k: v * factor for k, v in gemm.items()}
+        return factor, {k: v * factor for k, v in gemm.items()}, {k: v * factor for k, v in other.items()}
 
-    ff, fetch = read(fetch_dir, "FETCH_SIZE")
-    wf, write = read(write_dir, "WRITE_SIZE")
+    ff, fetch, fetch_o = read(fetch_dir, "FETCH_SIZE")
+    wf, write, write_o = read(write_dir, "WRITE_SIZE")
     cmd = ("rocprofv3 --pmc {c} --output-format csv -d {d} -o run -- python3 bench.py --config " + config +
            " --no-cpu-baseline --steps 3 --warmup 1 --copy-probe-mib " + str(probe_mib))
     rec = {"config": config, "ffn_source_hash": ffn_source_hash(),
@@ -119,7 +137,9 @@ def summarize_counters(config: str, fetch_dir: str, write_dir: str, probe_mib: i
            "fetch_factor": round(ff, 4), "write_factor": round(wf, 4),
            "fetch_bytes_per_launch": {k: round(v) for k, v in fetch.items()},
            "write_bytes_per_launch": {k: round(v) for k, v in write.items()},
-           "hbm_bytes_per_call": round(sum(fetch.values()) + sum(write.values()))}
+           "hbm_bytes_per_call": round(sum(fetch.values()) + sum(write.values())),
+           "other_steps_fetch_bytes_per_launch": {k: round(v) for k, v in fetch_o.items()},
+           "other_steps_write_bytes_per_launch": {k: round(v) for k, v in write_o.items()}}
     path = os.path.join(ROOT, "profiles", f"ffn_traffic_{config}.json")
     with open(path, "w") as fh:
         json.dump(rec, fh, indent=1)
@@ -423,6 +443,16 @@ def main():
                            "mfma_util": round(achieved_tflops / peak_tf, 4),
                            "hbm_frac": round(achieved_gbs / PEAK_HBM_GBS, 4)}
 
+    sb = stage_bytes(cfg, not args.unfused_gather, top1_fused, bias is not None and bias.dim() == 2)
+    stages_hbm = {}
+    for name, us in (("route", stage_us[0]), ("dispatch", stage_us[1]), ("combine", stage_us[3])):
+        if sb[name] and us > 0:
+            gbs = sb[name] / (us * 1e-6) / 1e9
+            stages_hbm[name] = {"bytes": sb[name], "us": round(us, 2), "gbs": round(gbs, 1),
+                                "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    stages_hbm["note"] = ("algorithmic bytes (inputs read once, outputs written once) over the stage's time in "
+                          "the untimed pass, launch gaps included, against 8 TB/s")
+
     out = {
         "metric": "MoE-layer tokens/sec on 1 MI355X; expert-GEMM MFMA util vs peak",
         "value": round(tokens_per_s, 1),
@@ -444,6 +474,7 @@ def main():
                       "expert_ffn": round(stage_us[2], 2), "combine": round(stage_us[3], 2),
                       "note": "separate untimed pass with events between calls" +
                               ("; top-1: the combine is part of the expert step" if top1_fused else "")},
+        "stages_hbm": stages_hbm,
         "expert_ffn_us_timed": round(ffn_us, 2),
         "timed_steps_us": {"expert_ffn": spread(ffn_each), "step": spread(step_each),
                            "note": "expert_ffn: the timed steps' events; step: a separate pass of "

@@ -184,3 +184,23 @@ def test_bench_names_the_expert_step_kernels():
     assert not bench.is_ffn_kernel("void moe::(anonymous namespace)::route_lds_kernel<1>(unsigned short const*)")
     assert [bench.ffn_matrix(n) for n in up] == ["up"] * 3
     assert [bench.ffn_matrix(n) for n in down] == ["down"] * 4
+    # the other layer steps are summarised separately; packing, casts and the probe are not steps
+    assert bench.is_layer_kernel("void moe::(anonymous namespace)::route_lds_kernel<1>(unsigned short const*)")
+    assert bench.is_layer_kernel("moe::(anonymous namespace)::dispatch_fused(int const*, long)")
+    assert bench.is_layer_kernel("void moe::(anonymous namespace)::combine_kernel<true, true>(void const*)")
+    assert not bench.is_layer_kernel("void moe::(anonymous namespace)::transpose_pad<unsigned short>(int)")
+    assert not bench.is_layer_kernel("void at::native::vectorized_elementwise_kernel<4, at::native::neg_kernel>")
+
+
+def test_bench_stage_bytes():
+    """Algorithmic bytes of the non-GEMM steps: inputs read once, outputs written once."""
+    import bench
+    import synth
+    c2, c5 = synth.CONFIGS["c2"], synth.CONFIGS["c5"]
+    b = bench.stage_bytes(c2, fused_gather=True, top1_fused=True, bias_per_row=True)
+    assert b["route"] == 8192 * 768 * 2 + 64 * 768 * 2 + 8192 * 64 * 4 + 8192 * 8
+    assert b["dispatch"] == 3 * 8192 * 4 + 129 * 4 and b["combine"] == 0
+    b = bench.stage_bytes(c5, fused_gather=False, top1_fused=False, bias_per_row=False)
+    A = 32768 * 2
+    assert b["dispatch"] == 3 * A * 4 + 129 * 4 + 2 * A * 1024 * 2
+    assert b["combine"] == A * 1024 * 2 + 32768 * 1024 * 2 + 32768 * 16
