@@ -204,3 +204,21 @@ def test_bench_stage_bytes():
     A = 32768 * 2
     assert b["dispatch"] == 3 * A * 4 + 129 * 4 + 2 * A * 1024 * 2
     assert b["combine"] == A * 1024 * 2 + 32768 * 1024 * 2 + 32768 * 16
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """Only one GPU is measured: --gpus above 1 exits with a message before touching a GPU."""
+    import subprocess
+    import sys
+    res = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                         text=True, timeout=120)
+    assert res.returncode == 2
+    assert "one GPU" in res.stderr and res.stdout == ""
+
+
+def test_bench_cpu_baseline_is_bounded():
+    """The oracle leg of the bench line: a bounded sample, its size and thread count stated."""
+    import bench
+    rec = bench.cpu_baseline("c1", 0, budget_s=2.0)
+    assert rec["kind"] == "oracle" and rec["unit"] == "tokens/s" and rec["value"] > 0
+    assert rec["cores"] >= 1 and "tokens of workload c1" in rec["sample"]
