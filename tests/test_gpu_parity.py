@@ -201,6 +201,22 @@ def test_ffn_parity(dtype, act, counts, h, f):
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("act", ["gelu", "swiglu"])
+@pytest.mark.parametrize("A,f", [(3000, 128), (300, 1024)])
+def test_ffn_parity_at_the_expert_limit(dtype, act, A, f):
+    """256 experts (the most the library takes), most of them with a handful of rows or none:
+    the row-tile table at its full size, in the grouped launch and, below 512 rows, with the
+    second product's K split."""
+    rng = np.random.default_rng(A + f)
+    counts = rng.multinomial(A, rng.dirichlet(np.full(256, 0.2))).tolist()
+    assert len(counts) == 256 and 0 in counts
+    x, w1, w3, w2, offsets = _ffn_case(rng, counts, 64, f, act, dtype)
+    got = _run_ffn(x, w1, w3, w2, offsets, act, dtype)
+    ref = oracle.expert_ffn(x, offsets, w1, w3, w2, act)
+    assert rowwise(got, ref) <= TOL[dtype], (rowwise(got, ref), normwise(got, ref))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("act", ["gelu", "swiglu"])
 @pytest.mark.parametrize("counts,h,f", [
     ([300, 0, 5, 129, 128, 1], 256, 200),
     ([0, 0, 77], 72, 128),
