@@ -199,6 +199,31 @@ def test_ffn_parity(dtype, act, counts, h, f):
     assert rowwise(got, ref) <= TOL[dtype], (rowwise(got, ref), normwise(got, ref))
 
 
+def _random_ffn_shapes(n, seed=2024):
+    rng = np.random.default_rng(seed)
+    shapes = []
+    for i in range(n):
+        E = int(rng.integers(1, 41))
+        A = int(rng.integers(0, 701))
+        counts = rng.multinomial(A, rng.dirichlet(np.full(E, 0.5))).tolist()
+        h = int(rng.choice([8, 64, 72, 136, 256, 520]))
+        f = int(rng.integers(1, 601))
+        shapes.append((i, counts, h, f, ["gelu", "gelu_tanh", "swiglu"][i % 3], ["bf16", "f32"][(i // 3) % 2]))
+    return shapes
+
+
+@pytest.mark.parametrize("i,counts,h,f,act,dtype", _random_ffn_shapes(12))
+def test_ffn_parity_on_random_shapes(i, counts, h, f, act, dtype):
+    """Seeded random shapes: expert count, ragged segments (some empty), hidden sizes off the
+    tile multiples, any inner width (split and unsplit second products)."""
+    rng = np.random.default_rng(100 + i)
+    x, w1, w3, w2, offsets = _ffn_case(rng, counts, h, f, act, dtype)
+    got = _run_ffn(x, w1, w3, w2, offsets, act, dtype)
+    ref = oracle.expert_ffn(x, offsets, w1, w3, w2, act)
+    if len(ref):
+        assert rowwise(got, ref) <= TOL[dtype], (rowwise(got, ref), normwise(got, ref))
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("act", ["gelu", "swiglu"])
 @pytest.mark.parametrize("A,f", [(3000, 128), (300, 1024)])
