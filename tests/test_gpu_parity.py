@@ -496,6 +496,31 @@ def test_layer_is_deterministic_with_split_k():
     assert torch.equal(y1, y2)
 
 
+@pytest.mark.parametrize("name,T", [("c5dec", None), ("c2", 1024)])
+def test_layer_replays_from_a_graph(name, T):
+    """A whole layer forward captured into a HIP graph (the library records no memset and
+    never synchronises) replays to the eager result, bit for bit, every time; eager work
+    clobbers the output between the replays."""
+    L = synth.make(name, seed=2, **({"T": T} if T else {}))
+    layer, x, bias, y_eager = _gpu_layer(L)
+    y_eager = y_eager.clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        layer(x, bias)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        y_graph = layer(x, bias)
+    for r in range(3):
+        layer.y.fill_(float(r + 1))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y_graph, y_eager), r
+
+
 def test_layer_with_no_tokens():
     L = synth.make("c2", seed=0, T=8, E=8)
     dt = torch.bfloat16
