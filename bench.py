@@ -3,7 +3,7 @@
 One step = one full layer forward (route -> dispatch -> expert FFN shard -> combine) over
 one batch of synthetic tokens already resident in HBM.  Prints one JSON line.
 
-  python bench.py [--steps K] [--warmup W] [--config c2] [--no-cpu-baseline] [--cold-steps N]
+  python bench.py [--steps K] [--warmup W] [--config c5] [--no-cpu-baseline] [--warm-steps N]
   python bench.py --ablation        # grouped vs per-expert launches, E = 8 .. 256
 
 HBM traffic of the expert-FFN kernels comes from two rocprofv3 counter runs of this script,
@@ -269,22 +269,34 @@ def cpu_baseline(cfg_name: str, seed: int, budget_s: float = 12.0):
     while dt * reps < budget_s / 4 and reps < 8:  # whole workload fits: repeat it for a steadier rate
         dt += run(n)
         reps += 1
-    return {"value": n * reps / dt, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+    return {"value": n * reps / dt, "unit": "tokens/s", "cores": oracle.num_threads(), "cpu": host_cpu_model(),
+            "kind": "oracle",
             "sample": f"first {n} of {cfg.T} tokens of workload {cfg_name} x{reps}, full layer "
                       f"(route, dispatch, expert FFN, combine) in fp64, {dt:.1f} s"}
+
+
+def host_cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=50,
-                    help="untimed steps first (the step time settles over the first few dozen)")
-    ap.add_argument("--config", default="c2")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="c5")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cold-steps", type=int, default=0,
-                    help="after the timed steps, this many more, each after a 512 MiB cache flush (cold_cache)")
+    ap.add_argument("--warm-steps", type=int, default=20,
+                    help="after the timed (cold-cache) steps, this many back-to-back steps with warm caches")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run an untimed plain copy of this size first (counter calibration)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
@@ -337,7 +349,7 @@ def main():
 
     def step(ev=None, ffn_ev=None):
         """One layer forward.  ev: 5 events around the four calls (stage breakdown);
-        ffn_ev: 2 events around the expert-FFN call only (kept in the timed loop)."""
+        ffn_ev: 2 events around the expert-FFN call only."""
         T, k = cfg.T, cfg.k
         if ev: ev[0].record(stream)
         moe.route(x, wg, k, bias, bool(cfg.renorm), out=(layer.idx, layer.w))
@@ -360,64 +372,79 @@ def main():
             moe.combine(layer.y_perm, layer.disp.pos_of, layer.w, out=layer.y)
         if ev: ev[4].record(stream)
 
-    for _ in range(args.warmup):
-        step()
-    ffn_events = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(ffn_ev=ffn_events[i])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ffn_each = np.array([a.elapsed_time(b) for a, b in ffn_events]) * 1e3
-    ffn_us = float(np.mean(ffn_each))
+    def new_events(n, m):
+        return [[torch.cuda.Event(enable_timing=True) for _ in range(m)] for _ in range(n)]
 
-    # per-step spread from a separate pass (an event between steps adds a little to each)
-    nspread = min(args.steps, 20)
-    step_events = [torch.cuda.Event(enable_timing=True) for _ in range(nspread + 1)]
-    for i in range(nspread):
-        step_events[i].record(stream)
-        step()
-    step_events[-1].record(stream)
-    torch.cuda.synchronize()
-    step_each = np.array([step_events[i].elapsed_time(step_events[i + 1]) for i in range(nspread)]) * 1e3
+    def us(pairs):
+        return np.array([a.elapsed_time(b) for a, b in pairs]) * 1e3
 
     def spread(v):
         return {"median": round(float(np.median(v)), 2), "p10": round(float(np.percentile(v, 10)), 2),
                 "p90": round(float(np.percentile(v, 90)), 2)}
 
-    # cold caches: a separate pass that overwrites 512 MiB (more than L2 and MALL together)
-    # before every step, outside the events
-    cold = None
-    if args.cold_steps:
-        scratch = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device=dev)
-        cev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.cold_steps)]
-        fev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.cold_steps)]
-        for i in range(args.cold_steps):
-            scratch.fill_(i & 0xff)
-            cev[i][0].record(stream)
-            step(ffn_ev=fev[i])
-            cev[i][1].record(stream)
+    # cache flush: 512 MiB written (more than L2 and MALL together), outside the step's events
+    scratch = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device=dev)
+
+    # untimed warm-up steps, each after a flush like the timed ones; their step times are kept
+    # (events around the step only) to show how the step time settles
+    wev = new_events(args.warmup, 2)
+    for i in range(args.warmup):
+        scratch.fill_(i & 0xff)
+        wev[i][0].record(stream)
+        step()
+        wev[i][1].record(stream)
+    torch.cuda.synchronize()
+    warm_curve = us(wev) if args.warmup else np.zeros(0)
+
+    # the timed steps: every step starts with cold caches (a flush before it, outside its
+    # events); value = tokens over the summed step times
+    sev, fev = new_events(args.steps, 2), new_events(args.steps, 2)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        scratch.fill_((i + 1) & 0xff)
+        sev[i][0].record(stream)
+        step(ffn_ev=fev[i])
+        sev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_each, ffn_each = us(sev), us(fev)
+    del scratch
+
+    # warm caches: back-to-back steps, wall clock (an extra figure, not the headline)
+    warm = None
+    if args.warm_steps:
+        wfe = new_events(args.warm_steps, 2)
         torch.cuda.synchronize()
-        cold = {"steps": args.cold_steps,
-                "step_us": spread(np.array([a.elapsed_time(b) for a, b in cev]) * 1e3),
-                "expert_ffn_us": spread(np.array([a.elapsed_time(b) for a, b in fev]) * 1e3),
-                "note": "512 MiB written before each step, outside the events"}
-        del scratch
+        tw = time.perf_counter()
+        for i in range(args.warm_steps):
+            step(ffn_ev=wfe[i])
+        torch.cuda.synchronize()
+        wall_w = time.perf_counter() - tw
+        warm = {"steps": args.warm_steps, "tokens_per_s": round(cfg.T * args.warm_steps / wall_w, 1),
+                "ms_per_step": round(wall_w / args.warm_steps * 1e3, 4),
+                "expert_ffn_us": spread(us(wfe)),
+                "note": "back-to-back steps without a flush, wall clock; inputs and weights partly in L2/MALL"}
 
     # stage breakdown from a separate, untimed pass (its events add gaps between calls)
     nbrk = min(args.steps, 10)
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(nbrk)]
+    events = new_events(nbrk, 5)
+    scratch = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device=dev)
     for i in range(nbrk):
+        scratch.fill_(i & 0xff)
         step(ev=events[i])
     torch.cuda.synchronize()
+    del scratch
     stage = np.zeros(4)
     for ev in events:
         for s in range(4):
             stage[s] += ev[s].elapsed_time(ev[s + 1])
     stage_us = stage / nbrk * 1e3
-    ms_per_step = wall / args.steps * 1e3
-    tokens_per_s = cfg.T * args.steps / wall
+
+    step_us = float(np.mean(step_each))
+    ms_per_step = step_us * 1e-3
+    tokens_per_s = cfg.T / (step_us * 1e-6)
+    ffn_us = float(np.mean(ffn_each))
 
     counts = layer.disp.counts.cpu().numpy()
     A, h, f = cfg.A, cfg.h, cfg.f
@@ -438,20 +465,21 @@ def main():
     roof["traffic"] = measured_traffic(args.config)
     roof["kernel"] = ("moe_expert_ffn_shard" + ("_top1" if top1_fused else "" if args.unfused_gather else "_gather") +
                       " (grouped GEMM1+act and GEMM2, one launch each; calls of at most 512 bf16 rows"
-                      " add one launch that sums the K parts of GEMM2)")
+                      " add one launch that sums the K parts of GEMM2); HIP events around the call in every "
+                      "timed (cold-cache) step")
     roof["algorithmic"] = {"bytes": ffn_bytes, "flops": ffn_flops, "touched_experts": touched,
                            "mfma_util": round(achieved_tflops / peak_tf, 4),
                            "hbm_frac": round(achieved_gbs / PEAK_HBM_GBS, 4)}
 
     sb = stage_bytes(cfg, not args.unfused_gather, top1_fused, bias is not None and bias.dim() == 2)
     stages_hbm = {}
-    for name, us in (("route", stage_us[0]), ("dispatch", stage_us[1]), ("combine", stage_us[3])):
-        if sb[name] and us > 0:
-            gbs = sb[name] / (us * 1e-6) / 1e9
-            stages_hbm[name] = {"bytes": sb[name], "us": round(us, 2), "gbs": round(gbs, 1),
+    for name, t_us in (("route", stage_us[0]), ("dispatch", stage_us[1]), ("combine", stage_us[3])):
+        if sb[name] and t_us > 0:
+            gbs = sb[name] / (t_us * 1e-6) / 1e9
+            stages_hbm[name] = {"bytes": sb[name], "us": round(t_us, 2), "gbs": round(gbs, 1),
                                 "frac": round(gbs / PEAK_HBM_GBS, 4)}
     stages_hbm["note"] = ("algorithmic bytes (inputs read once, outputs written once) over the stage's time in "
-                          "the untimed pass, launch gaps included, against 8 TB/s")
+                          "the untimed pass (cold caches, events between calls), against 8 TB/s")
 
     out = {
         "metric": "MoE-layer tokens/sec on 1 MI355X; expert-GEMM MFMA util vs peak",
@@ -470,19 +498,22 @@ def main():
                                f"({cfg.act}), routing {cfg.routing[0]}",
                    "tokens": cfg.T, "hidden": h, "experts": cfg.E, "top_k": cfg.k, "shard_inner_width": f,
                    "parallelism": "single device"},
+        "timing": ("cold caches: 512 MiB written before every timed step, outside HIP events that bracket the "
+                   "step; value = tokens / mean step time; wall clock of the timed loop (flushes included) "
+                   f"{wall * 1e3:.2f} ms"),
         "stages_us": {"route": round(stage_us[0], 2), "dispatch": round(stage_us[1], 2),
                       "expert_ffn": round(stage_us[2], 2), "combine": round(stage_us[3], 2),
                       "note": "separate untimed pass with events between calls" +
                               ("; top-1: the combine is part of the expert step" if top1_fused else "")},
         "stages_hbm": stages_hbm,
         "expert_ffn_us_timed": round(ffn_us, 2),
-        "timed_steps_us": {"expert_ffn": spread(ffn_each), "step": spread(step_each),
-                           "note": "expert_ffn: the timed steps' events; step: a separate pass of "
-                                   f"{nspread} steps with an event between steps"},
+        "timed_steps_us": {"step": spread(step_each), "expert_ffn": spread(ffn_each)},
+        "warmup_steps_us": {"first": [round(float(v), 1) for v in warm_curve[:5]],
+                            "last5_median": round(float(np.median(warm_curve[-5:])), 1) if len(warm_curve) else None},
         "roofline": roof,
     }
-    if cold is not None:
-        out["cold_cache"] = cold
+    if warm is not None:
+        out["warm_cache"] = warm
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.config, args.seed)
     print(json.dumps(out), flush=True)

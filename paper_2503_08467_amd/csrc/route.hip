@@ -230,14 +230,12 @@ __global__ __launch_bounds__(kWaves * kWave) void route_lds_kernel(const bf16_t*
     }
     const unsigned char* xb = uniform_ptr(reinterpret_cast<const unsigned char*>(x + tok0 * h));
     const unsigned char* gb = uniform_ptr(reinterpret_cast<const unsigned char*>(wg));
-    // workgroups start at different K chunks (and wrap around), so that they do not all read
-    // the same gate rows at the same moment; a token's sum order is still fixed
-    const int rot = static_cast<int>(blockIdx.x % static_cast<unsigned>(nk));
+    // every workgroup walks K in the same order, so a token's logits are summed in the same
+    // order wherever it sits in the batch (its picks do not depend on T or its position)
     int issued = 0;
     auto issue = [&]() {
         const uint32_t dst = lds0 + (issued % NS) * S::kChunkBytes;
-        const int c = issued + rot < nk ? issued + rot : issued + rot - nk;
-        const int kb = c * kRK * 2;
+        const int kb = issued * kRK * 2;
 #pragma unroll
         for (int j = 0; j < LPW; ++j)
             load_lds16((j < kXJ ? xb : gb) + kb, voff[j], dst + (4 * j + wave) * 1024);

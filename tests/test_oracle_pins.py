@@ -100,6 +100,23 @@ def test_gelu_tanh_is_within_published_deviation_of_gelu():
     assert t[400] == 0.0 and g[400] == 0.0  # u = 0
 
 
+def test_gelu_tanh_against_torch_float64():
+    """The tanh form against an independent implementation of the same published formula
+    (PyTorch's GELU with approximate="tanh", evaluated in float64 on the CPU): a slip in
+    either coefficient (sqrt(2/pi), 0.044715) moves values far more than rounding."""
+    torch = pytest.importorskip("torch")
+    u = np.concatenate([np.linspace(-8, 8, 1601), [-0.75, 0.3, 1.7, 2.9]]).astype(np.float32)[:, None]
+    one = np.ones((1, 1, 1), np.float32)
+    e = np.zeros(u.shape[0], np.int32)
+    t = oracle.ffn_rows(u, e, one, None, one, "gelu_tanh")[:, 0]
+    ref = torch.nn.functional.gelu(torch.from_numpy(u[:, 0].astype(np.float64)), approximate="tanh").numpy()
+    np.testing.assert_allclose(t, ref, rtol=1e-13, atol=1e-15)
+    # sensitivity: 0.0447 instead of 0.044715 would differ by more than 1e-6 near |u| = 2
+    c = math.sqrt(2.0 / math.pi)
+    slip = 0.5 * u[:, 0] * (1.0 + np.tanh(c * (u[:, 0] + 0.0447 * u[:, 0] ** 3)))
+    assert np.max(np.abs(slip - ref)) > 1e-6
+
+
 # ---------------------------------------------------------------- P1: dense == sparse
 
 @settings(max_examples=25, deadline=None)
