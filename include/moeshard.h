@@ -49,8 +49,13 @@ typedef enum {
     MOE_ERR_INVALID_ARG = 1, /* a size, pointer, alignment or enum value is invalid */
     MOE_ERR_UNSUPPORTED = 2, /* valid request this build does not implement */
     MOE_ERR_WORKSPACE = 3,   /* the workspace or packed buffer is too small */
-    MOE_ERR_HIP = 4          /* the HIP runtime reported a launch error */
+    MOE_ERR_HIP = 4,         /* the HIP runtime reported a launch error */
+    MOE_ERR_TOO_LARGE = 5    /* the call needs more than MOE_NOALLOC_SCRATCH_BYTES of scratch
+                                (moe_expert_ffn_shard_noalloc only) */
 } moe_status;
+
+/* Bytes of the static per-device scratch array behind moe_expert_ffn_shard_noalloc. */
+#define MOE_NOALLOC_SCRATCH_BYTES (64u * 1024u * 1024u)
 
 typedef enum { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype;
 
@@ -203,6 +208,26 @@ moe_status moe_expert_ffn_shard_per_expert(const void *x_perm, const int32_t *of
                                            int64_t h, int64_t f, moe_act act, moe_dtype dt,
                                            const void *packed, void *y_perm, moe_dtype ydt,
                                            void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* For callers that cannot allocate device memory -- code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc: moe_expert_ffn_shard with the same
+ * arguments, result and bits, but with no caller workspace.  The scratch it needs (the
+ * activated inner rows and, for A_max <= 512 in bf16, the partial sums of the second
+ * product) lives in a static device array of MOE_NOALLOC_SCRATCH_BYTES that the library
+ * holds on every GPU it runs on until the process ends.  The call itself allocates and
+ * frees nothing; its first call on a device looks up that device's copy of the array
+ * (hipGetSymbolAddress) once.
+ *   Limit: moe_ffn_workspace_size(A_max, E, h, f, act, dt) must not exceed
+ *          MOE_NOALLOC_SCRATCH_BYTES, else MOE_ERR_TOO_LARGE and nothing is launched
+ *          (e.g. bf16 with f = 4096 takes A_max up to about 8000 rows).
+ *   stream must belong to the current device (else MOE_ERR_HIP, nothing launched).
+ *   Every call on one GPU uses the same array: calls that may overlap on one GPU (other
+ *   streams, other threads) race and give wrong results; order them on one stream.  The
+ *   array keeps the last call's contents; no call depends on them. */
+moe_status moe_expert_ffn_shard_noalloc(const void *x_perm, const int32_t *offsets, int64_t A_max,
+                                        int32_t E, int64_t h, int64_t f, moe_act act, moe_dtype dt,
+                                        const void *packed, void *y_perm, moe_dtype ydt,
+                                        hipStream_t stream);
 
 /* Step 5 (Algorithm 1, aggregateTokens): point-wise weighted sum of each token's expert
  * results, accumulated in fp32 in pick order j = 0..k-1 and rounded once:

@@ -11,7 +11,8 @@ import threading
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmoeshard.so")
 
-MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP = range(5)
+MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP, MOE_ERR_TOO_LARGE = range(6)
+MOE_NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024
 MOE_F32, MOE_BF16 = 0, 1
 MOE_ACT_GELU, MOE_ACT_GELU_TANH, MOE_ACT_SWIGLU = 0, 1, 2
 MOE_MAX_EXPERTS = 256
@@ -36,6 +37,7 @@ SIGNATURES = {
     "moe_expert_ffn_shard_top1": (_ST, [_P, _I64, _P, _P, _P, _I32, _I64, _I64, _ST, _ST, _P, _P, _ST, _P, _SZ, _P]),
     "moe_expert_ffn_shard_per_expert": (_ST, [_P, _P, _P, _I64, _I32, _I64, _I64, _ST, _ST, _P, _P, _ST, _P, _SZ,
                                               _P]),
+    "moe_expert_ffn_shard_noalloc": (_ST, [_P, _P, _I64, _I32, _I64, _I64, _ST, _ST, _P, _P, _ST, _P]),
     "moe_combine": (_ST, [_P, _ST, _P, _P, _I64, _I32, _I64, _P, _ST, _P]),
 }
 

@@ -43,6 +43,7 @@ const char* moe_status_string(moe_status status) {
         case MOE_ERR_UNSUPPORTED: return "MOE_ERR_UNSUPPORTED: request not implemented in this build";
         case MOE_ERR_WORKSPACE: return "MOE_ERR_WORKSPACE: workspace or packed buffer too small";
         case MOE_ERR_HIP: return "MOE_ERR_HIP: HIP runtime error at launch";
+        case MOE_ERR_TOO_LARGE: return "MOE_ERR_TOO_LARGE: the call needs more than the static scratch array holds";
     }
     return "unknown moe_status";
 }
@@ -132,18 +133,27 @@ size_t moe_ffn_workspace_size(int64_t A_max, int32_t E, int64_t h, int64_t f, mo
            align_up(moe::down_partial_bytes(A_max, h, fp, dt == MOE_BF16)) + kAlign;
 }
 
-static moe_status ffn_check(const void* x_perm, const int32_t* offsets, int64_t A_max, int32_t E, int64_t h,
-                            int64_t f, moe_act act, moe_dtype dt, const void* packed, const void* y_perm,
-                            moe_dtype ydt, const void* ws, size_t ws_bytes) {
+// Checks shared by the expert-step calls, all but the workspace.
+static moe_status ffn_args_check(const void* x_perm, const int32_t* offsets, int64_t A_max, int32_t E, int64_t h,
+                                 int64_t f, moe_act act, moe_dtype dt, const void* packed, const void* y_perm,
+                                 moe_dtype ydt) {
     if (!valid_dtype(dt) || !valid_dtype(ydt) || !valid_act(act) || !valid_h(h) || E < 1 || f < 1 || A_max < 0)
         return MOE_ERR_INVALID_ARG;
     if (E > MOE_MAX_EXPERTS) return MOE_ERR_UNSUPPORTED;
     if (A_max >= INT32_MAX) return MOE_ERR_INVALID_ARG;
     if (moe_padded_inner_width(f) >= INT32_MAX / 2) return MOE_ERR_UNSUPPORTED;
     const bool any = A_max > 0;
-    if (!ok_ptr(x_perm, any) || !ok_ptr(offsets, true) || !ok_ptr(packed, true) || !ok_ptr(y_perm, any) ||
-        !ok_ptr(ws, any))
+    if (!ok_ptr(x_perm, any) || !ok_ptr(offsets, true) || !ok_ptr(packed, true) || !ok_ptr(y_perm, any))
         return MOE_ERR_INVALID_ARG;
+    return MOE_OK;
+}
+
+static moe_status ffn_check(const void* x_perm, const int32_t* offsets, int64_t A_max, int32_t E, int64_t h,
+                            int64_t f, moe_act act, moe_dtype dt, const void* packed, const void* y_perm,
+                            moe_dtype ydt, const void* ws, size_t ws_bytes) {
+    const moe_status st = ffn_args_check(x_perm, offsets, A_max, E, h, f, act, dt, packed, y_perm, ydt);
+    if (st != MOE_OK) return st;
+    if (!ok_ptr(ws, A_max > 0)) return MOE_ERR_INVALID_ARG;
     if (ws_bytes < moe_ffn_workspace_size(A_max, E, h, f, act, dt)) return MOE_ERR_WORKSPACE;
     return MOE_OK;
 }
@@ -222,6 +232,24 @@ moe_status moe_expert_ffn_shard_per_expert(const void* x_perm, const int32_t* of
     return from_hip(moe::launch_ffn_per_expert(x_perm, offsets, offsets_host, A_max, E, static_cast<int>(h),
                                                moe_padded_inner_width(f), static_cast<int>(act), dt == MOE_BF16, w1t,
                                                w3t, w2t, y_perm, ydt == MOE_BF16, ws, stream));
+}
+
+moe_status moe_expert_ffn_shard_noalloc(const void* x_perm, const int32_t* offsets, int64_t A_max, int32_t E,
+                                        int64_t h, int64_t f, moe_act act, moe_dtype dt, const void* packed,
+                                        void* y_perm, moe_dtype ydt, hipStream_t stream) {
+    // the argument checks of moe_expert_ffn_shard; the static array is the workspace
+    const moe_status st = ffn_args_check(x_perm, offsets, A_max, E, h, f, act, dt, packed, y_perm, ydt);
+    if (st != MOE_OK) return st;
+    if (moe_ffn_workspace_size(A_max, E, h, f, act, dt) > MOE_NOALLOC_SCRATCH_BYTES) return MOE_ERR_TOO_LARGE;
+    const size_t mb = packed_matrix_bytes(E, h, f, dt);
+    const unsigned char* base = static_cast<const unsigned char*>(packed);
+    const bool swiglu = act == MOE_ACT_SWIGLU;
+    const void* w1t = base;
+    const void* w3t = swiglu ? base + mb : nullptr;
+    const void* w2t = base + (swiglu ? 2 : 1) * mb;
+    return from_hip(moe::launch_ffn_noalloc(x_perm, offsets, A_max, E, static_cast<int>(h),
+                                            moe_padded_inner_width(f), static_cast<int>(act), dt == MOE_BF16, w1t,
+                                            w3t, w2t, y_perm, ydt == MOE_BF16, stream));
 }
 
 moe_status moe_combine(const void* y_perm, moe_dtype ydt, const int32_t* pos_of, const float* topk_w, int64_t T,

@@ -1457,6 +1457,61 @@ hipError_t launch_ffn_top1(const void* x, int64_t T, const int32_t* row_src, con
                     topk_w);
 }
 
+// ------------------------------------------------------------------ no-allocation variant
+//
+// The workspace of one call (H, then the split second product's partial tiles) lives in a
+// static device array instead of caller memory.  Each GPU the library runs on holds its own
+// copy of the array for the life of the process.  In host code the array's name only stands
+// in for it: the device address comes from hipGetSymbolAddress, taken once per device with
+// that device current, and only that address is ever handed to a kernel.  Nothing in the
+// array needs to start at zero (every H row and partial tile a kernel reads is written
+// earlier in the same call; rows of a tile past its segment only feed outputs that are not
+// stored).  Calls that overlap on one GPU share the array and race.
+namespace {
+
+__device__ __align__(256) unsigned char scratch[MOE_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// Device address of `scratch` on the current device (resolved on the first call there).
+hipError_t static_scratch(void** out) {
+    int dev = -1;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return err;
+    if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (err != hipSuccess) return err;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_ffn_noalloc(const void* x_perm, const int32_t* offsets, int64_t A_max, int E, int h, int64_t fp,
+                              int act, bool bf16, const void* w1t, const void* w3t, const void* w2t, void* y_perm,
+                              bool y_bf16, hipStream_t s) {
+    if (s) {  // the stream must belong to the current device, whose copy of the array is used
+        int sdev = -1, dev = -1;
+        hipError_t err = hipStreamGetDevice(s, &sdev);
+        if (err != hipSuccess) return err;
+        err = hipGetDevice(&dev);
+        if (err != hipSuccess) return err;
+        if (sdev != dev) return hipErrorInvalidDevice;
+    }
+    void* ws = nullptr;
+    const hipError_t err = static_scratch(&ws);
+    if (err != hipSuccess) return err;
+    return ffn_pair(x_perm, offsets, A_max, A_max, E, h, fp, act, bf16, w1t, w3t, w2t, y_perm, y_bf16, ws, s);
+}
+
 hipError_t launch_ffn_per_expert(const void* x_perm, const int32_t* offsets, const int32_t* offsets_host,
                                  int64_t A_max, int E, int h, int64_t fp, int act, bool bf16, const void* w1t,
                                  const void* w3t, const void* w2t, void* y_perm, bool y_bf16, void* hbuf,

@@ -68,6 +68,11 @@ hipError_t launch_ffn_per_expert(const void* x_perm, const int32_t* offsets, con
                                  const void* w3t, const void* w2t, void* y_perm, bool y_bf16, void* hbuf,
                                  hipStream_t s);
 
+// moe_expert_ffn_shard with its workspace in the library's static per-device array.
+hipError_t launch_ffn_noalloc(const void* x_perm, const int32_t* offsets, int64_t A_max, int E, int h, int64_t fp,
+                              int act, bool bf16, const void* w1t, const void* w3t, const void* w2t, void* y_perm,
+                              bool y_bf16, hipStream_t s);
+
 hipError_t launch_combine(const void* y_perm, bool y_bf16, const int32_t* pos_of, const float* w,
                           int64_t T, int k, int h, void* y, bool out_bf16, hipStream_t s);
 

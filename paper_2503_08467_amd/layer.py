@@ -176,6 +176,23 @@ def expert_ffn_shard(x_perm: torch.Tensor, offsets: torch.Tensor, packed: Packed
     return out
 
 
+def expert_ffn_shard_noalloc(x_perm: torch.Tensor, offsets: torch.Tensor, packed: PackedShard,
+                             out: torch.Tensor, A_max: Optional[int] = None, stream=None) -> torch.Tensor:
+    """Step 4 as expert_ffn_shard, with no workspace: the library's static per-device scratch
+    array holds it (calls on one GPU must not overlap).  The caller passes the output."""
+    _dev(x_perm, "x_perm"), _dev(offsets, "offsets"), _dev(out, "out")
+    if x_perm.dtype != packed.dtype:
+        raise TypeError("x_perm must have the packed weights' dtype")
+    A = x_perm.shape[0]
+    A_max = A if A_max is None else A_max
+    if A_max > A or out.shape != (A, packed.h):
+        raise ValueError("A_max exceeds the rows of x_perm, or out is not [A, h]")
+    _lib.call("moe_expert_ffn_shard_noalloc", _ptr(x_perm), _ptr(offsets), A_max, packed.E, packed.h, packed.f,
+              _lib.ACTS[packed.act], _DT[packed.dtype], _ptr(packed.buf), _ptr(out), _dt(out),
+              _stream(x_perm, stream))
+    return out
+
+
 def expert_ffn_shard_gather(x: torch.Tensor, row_src: torch.Tensor, offsets: torch.Tensor, packed: PackedShard,
                             out_dtype: Optional[torch.dtype] = None, A_max: Optional[int] = None,
                             out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,

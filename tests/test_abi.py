@@ -30,14 +30,14 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 13, names
+    assert len(names) == 14, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(_lib.SIGNATURES)
 
 
 def test_status_strings(lib):
-    for st in range(5):
+    for st in range(6):
         assert _lib.status_string(st).startswith("MOE_")
     assert "unknown" in _lib.status_string(99)
 
@@ -222,3 +222,20 @@ def test_bench_cpu_baseline_is_bounded():
     rec = bench.cpu_baseline("c1", 0, budget_s=2.0)
     assert rec["kind"] == "oracle" and rec["unit"] == "tokens/s" and rec["value"] > 0
     assert rec["cores"] >= 1 and "tokens of workload c1" in rec["sample"]
+
+
+def test_noalloc_rejects_calls_beyond_its_static_array(lib):
+    """The no-allocation expert step refuses, before touching the GPU, a call whose scratch
+    would not fit the static array; a call that fits passes validation (not run here)."""
+    h, f, E = 64, 4096, 2
+    big, small = 10000, 4000
+    assert lib.moe_ffn_workspace_size(big, E, h, f, _lib.MOE_ACT_GELU, _lib.MOE_BF16) > _lib.MOE_NOALLOC_SCRATCH_BYTES
+    assert lib.moe_ffn_workspace_size(small, E, h, f, _lib.MOE_ACT_GELU, _lib.MOE_BF16) <= \
+        _lib.MOE_NOALLOC_SCRATCH_BYTES
+    st = lib.moe_expert_ffn_shard_noalloc(A16, A16, big, E, h, f, _lib.MOE_ACT_GELU, _lib.MOE_BF16, A16, A16,
+                                          _lib.MOE_BF16, None)
+    assert st == _lib.MOE_ERR_TOO_LARGE
+    # ordinary argument errors come first
+    st = lib.moe_expert_ffn_shard_noalloc(A16 + 4, A16, big, E, h, f, _lib.MOE_ACT_GELU, _lib.MOE_BF16, A16, A16,
+                                          _lib.MOE_BF16, None)
+    assert st == _lib.MOE_ERR_INVALID_ARG
