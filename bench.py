@@ -244,8 +244,10 @@ def ablation_per_expert(seed: int, reps: int, experts):
         torch.cuda.empty_cache()
 
 
-def cpu_baseline(cfg_name: str, seed: int, budget_s: float = 12.0):
-    """The fp64 oracle on a bounded sample of the same workload (its first tokens)."""
+def cpu_baseline(cfg_name: str, seed: int, budget_s: float = 40.0):
+    """The fp64 oracle on a bounded sample of the same workload (its first tokens): the
+    sample grows until one run takes a quarter of budget_s, then repeats until the total
+    reaches it (about 10-20 s of CPU work)."""
     import oracle
     cfg = synth.CONFIGS[cfg_name]
     L = synth.make(cfg_name, seed=seed)
@@ -266,7 +268,7 @@ def cpu_baseline(cfg_name: str, seed: int, budget_s: float = 12.0):
         n = min(cfg.T, max(2 * n, int(n * (budget_s / 2) / max(dt, 1e-3))))
         dt = run(n)
     reps = 1
-    while dt * reps < budget_s / 4 and reps < 8:  # whole workload fits: repeat it for a steadier rate
+    while dt < budget_s / 4 and reps < 8:  # whole workload fits: repeat it for a steadier rate
         dt += run(n)
         reps += 1
     return {"value": n * reps / dt, "unit": "tokens/s", "cores": oracle.num_threads(), "cpu": host_cpu_model(),

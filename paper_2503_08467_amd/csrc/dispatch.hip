@@ -10,10 +10,11 @@
 //           assignment's position is   chunk base + earlier waves' count + running count
 //           + number of lower lanes with the same expert   -- stable in (t, j) order
 //   gather  x_perm[p] = x[row_src[p]] with 16-byte vector copies
-// Up to kFusedMaxA assignments, count, scan and rank run as one kernel instead (same
-// output): every chunk's workgroup counts all assignments itself into per-wave LDS
-// histograms, keeping the counts of the chunks before its own apart, scans the totals,
-// and ranks its chunk as above.  Three dependent launches of a few microseconds each become one.
+// When the count table (experts x chunks) is small, the scan runs inside every rank
+// workgroup instead (dispatch_rank_scan: two launches).  Up to kFusedMaxA assignments,
+// count, scan and rank run as one kernel (same output): every chunk's workgroup counts all
+// assignments itself into per-wave LDS histograms, keeping the counts of the chunks before
+// its own apart, scans the totals, and ranks its chunk as above.
 // Integer atomics are used only for the LDS histograms, whose result does not depend on
 // their order.
 #include "common.h"
@@ -108,6 +109,123 @@ __global__ __launch_bounds__(kDispThreads) void dispatch_rank(const int32_t* __r
     __syncthreads();
     for (int e = lane; e < E; e += kWave) {
         int b = base[static_cast<int64_t>(e) * nchunks + c];
+        for (int w = 0; w < wave; ++w) b += wcnt[w][e];
+        run[wave][e] = b;
+    }
+    __syncthreads();
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
+    for (int s = 0; s < kRounds; ++s) {
+        const int64_t a = a0 + s * kWave + lane;
+        const int e = ev[s];
+        const bool valid = static_cast<unsigned>(e) < static_cast<unsigned>(E);
+        uint64_t peers = __ballot(valid);
+        for (int b = 0; b < nbits; ++b) {
+            const bool bit = valid && ((e >> b) & 1);
+            const uint64_t m = __ballot(bit);
+            peers &= bit ? m : ~m;
+        }
+        const int rank = __popcll(peers & lt);
+        if (valid) {
+            const int pos = run[wave][e] + rank;
+            pos_of[a] = pos;
+            if (pos >= 0 && pos < A) row_src[pos] = static_cast<int32_t>(a / k);
+        } else if (a < A) {
+            pos_of[a] = -1;
+        }
+        __syncthreads();  // every lane has read run[] before the group leaders advance it
+        if (valid && rank == 0) run[wave][e] += __popcll(peers);
+        __syncthreads();
+    }
+}
+
+// Rank with the scan folded in (two launches instead of three, for count tables that fit
+// kRankScanMaxTable entries of LDS): every chunk's workgroup reads the whole table cc, sums each
+// expert's row (the totals, and separately the chunks before its own), scans the totals, and
+// ranks its chunk from base = offsets[e] + (earlier chunks' count of e).  Workgroup 0 writes
+// counts and offsets.
+constexpr int64_t kRankScanMaxTable = 8192;
+
+__global__ __launch_bounds__(kDispThreads) void dispatch_rank_scan(const int32_t* __restrict__ idx, int64_t A,
+                                                                   int k, int E, int nbits, int nchunks,
+                                                                   const int32_t* __restrict__ cc,
+                                                                   int32_t* __restrict__ counts,
+                                                                   int32_t* __restrict__ offsets,
+                                                                   int32_t* __restrict__ row_src,
+                                                                   int32_t* __restrict__ pos_of) {
+    __shared__ int table[kRankScanMaxTable];
+    __shared__ int tot[MOE_MAX_EXPERTS];
+    __shared__ int before[MOE_MAX_EXPERTS];
+    __shared__ int off[MOE_MAX_EXPERTS + 1];
+    __shared__ int wcnt[kDispWaves][MOE_MAX_EXPERTS];
+    __shared__ int run[kDispWaves][MOE_MAX_EXPERTS];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int c = blockIdx.x;
+    const int64_t a0 = static_cast<int64_t>(c) * kDispatchChunk + wave * kPerWave;
+    // this chunk's ids and the whole count table, loaded together (one memory round trip)
+    int ev[kRounds];
+#pragma unroll
+    for (int s = 0; s < kRounds; ++s) {
+        const int64_t a = a0 + s * kWave + lane;
+        ev[s] = (a < A) ? idx[a] : -1;
+    }
+    // stored chunk-major with a padded row (E + 1 counters), so that both the copy and the
+    // per-expert sums below touch distinct banks
+    const int L = E * nchunks;
+    for (int i = threadIdx.x; i < L; i += kDispThreads) {
+        const int e = i / nchunks, ch = i - e * nchunks;
+        table[ch * (E + 1) + e] = cc[i];
+    }
+    for (int e = lane; e < E; e += kWave) wcnt[wave][e] = 0;
+    __syncthreads();
+    static_assert(MOE_MAX_EXPERTS <= kDispThreads, "one expert per thread");
+    if (threadIdx.x < E) {
+        int t = 0, b = 0;
+        for (int i = 0; i < nchunks; ++i) {
+            const int v = table[i * (E + 1) + threadIdx.x];
+            t += v;
+            b += i < c ? v : 0;
+        }
+        tot[threadIdx.x] = t;
+        before[threadIdx.x] = b;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int s = 0; s < kRounds; ++s)
+        if (static_cast<unsigned>(ev[s]) < static_cast<unsigned>(E)) atomicAdd(&wcnt[wave][ev[s]], 1);
+    // exclusive scan of the totals: one wave, four experts per lane
+    static_assert(MOE_MAX_EXPERTS == 4 * kWave, "four experts per lane of one wave");
+    if (wave == 0) {
+        int ex[4], sum = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int e = lane * 4 + i;
+            ex[i] = sum;
+            sum += (e < E) ? tot[e] : 0;
+        }
+        int incl = sum;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const int t = __shfl_up(incl, o, kWave);
+            if (lane >= o) incl += t;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int e = lane * 4 + i;
+            if (e < E) off[e] = incl - sum + ex[i];
+        }
+        if (lane == kWave - 1) off[E] = incl;
+    }
+    __syncthreads();
+    if (c == 0) {
+        for (int e = threadIdx.x; e <= E; e += kDispThreads) {
+            offsets[e] = off[e];
+            if (e < E) counts[e] = tot[e];
+        }
+    }
+    for (int e = lane; e < E; e += kWave) {
+        int b = off[e] + before[e];
         for (int w = 0; w < wave; ++w) b += wcnt[w][e];
         run[wave][e] = b;
     }
@@ -319,11 +437,16 @@ hipError_t launch_dispatch(const int32_t* idx, int64_t T, int k, int E, const vo
         if (nchunks > 0) {
             hipLaunchKernelGGL(dispatch_count, dim3(nchunks), dim3(kDispThreads), 0, s, idx, A, E, nchunks, cc);
         }
-        hipLaunchKernelGGL(dispatch_scan, dim3(1), dim3(kScanThreads), 0, s, cc, E, nchunks, base, counts,
-                           offsets);
-        if (nchunks > 0) {
-            hipLaunchKernelGGL(dispatch_rank, dim3(nchunks), dim3(kDispThreads), 0, s, idx, A, k, E, nbits,
-                               nchunks, base, row_src, pos_of);
+        if (nchunks > 0 && static_cast<int64_t>(E + 1) * nchunks <= kRankScanMaxTable) {
+            hipLaunchKernelGGL(dispatch_rank_scan, dim3(nchunks), dim3(kDispThreads), 0, s, idx, A, k, E, nbits,
+                               nchunks, cc, counts, offsets, row_src, pos_of);
+        } else {
+            hipLaunchKernelGGL(dispatch_scan, dim3(1), dim3(kScanThreads), 0, s, cc, E, nchunks, base, counts,
+                               offsets);
+            if (nchunks > 0) {
+                hipLaunchKernelGGL(dispatch_rank, dim3(nchunks), dim3(kDispThreads), 0, s, idx, A, k, E, nbits,
+                                   nchunks, base, row_src, pos_of);
+            }
         }
     }
     if (nchunks > 0) {

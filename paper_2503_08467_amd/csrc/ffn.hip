@@ -369,25 +369,21 @@ struct LdsShape {
 
 // Stores one lane's share of a 32 x 32 bf16 output block.  The MFMA layout leaves lane
 // (row, half) with columns 8 q + 4 half .. 8 q + 4 half + 3 of its row, q = 0..3, packed
-// as pk[q].  Lanes l and l ^ 32 hold the same row; they swap two of their four groups, so
-// that each then holds two runs of 8 consecutive columns, 8 half .. 8 half + 7 and 16 +
-// 8 half .. 16 + 8 half + 7, stored as one 16-byte vector each: half the store
-// instructions of 8-byte groups, and 32 contiguous bytes of every row per instruction.
-// dst = the lane's row at column 8 half of the block (the second run is dst + 16); ok0 /
-// ok1 say whether each run is stored.  Every lane of the wave must call it (the swap).
-__device__ __forceinline__ void store_block_bf16(bf16_t* dst, const uint2 (&pk)[4], int lhi, bool ok0, bool ok1) {
-    const uint2 ga = lhi ? pk[0] : pk[1], gb = lhi ? pk[2] : pk[3];
-    uint2 ra, rb;
-    ra.x = __shfl_xor(ga.x, 32, kWave);
-    ra.y = __shfl_xor(ga.y, 32, kWave);
-    rb.x = __shfl_xor(gb.x, 32, kWave);
-    rb.y = __shfl_xor(gb.y, 32, kWave);
-    if (ok0)
-        *reinterpret_cast<uint4*>(dst) =
-            lhi ? make_uint4(ra.x, ra.y, pk[1].x, pk[1].y) : make_uint4(pk[0].x, pk[0].y, ra.x, ra.y);
-    if (ok1)
-        *reinterpret_cast<uint4*>(dst + 16) =
-            lhi ? make_uint4(rb.x, rb.y, pk[3].x, pk[3].y) : make_uint4(pk[2].x, pk[2].y, rb.x, rb.y);
+// as pk[q].  Lanes l and l + 32 hold the same row; v_permlane32_swap trades lane l's pk[1]
+// for lane l + 32's pk[0] (and pk[3] for pk[2]), after which lane l holds columns 0..7 and
+// 16..23 of the row and lane l + 32 columns 8..15 and 24..31, each run stored as one
+// 16-byte vector: half the store instructions of 8-byte groups, and 32 contiguous bytes of
+// every row per instruction.  dst = the lane's row at column 8 half of the block (the
+// second run is dst + 16); ok0 / ok1 say whether each run is stored.  Every lane of the
+// wave must call it (the swap).
+__device__ __forceinline__ void store_block_bf16(bf16_t* dst, const uint2 (&pk)[4], bool ok0, bool ok1) {
+    // swap(vdst, src): lanes 32..63 of vdst <-> lanes 0..31 of src; returns {vdst, src}
+    const auto a0 = __builtin_amdgcn_permlane32_swap(pk[0].x, pk[1].x, false, false);
+    const auto a1 = __builtin_amdgcn_permlane32_swap(pk[0].y, pk[1].y, false, false);
+    const auto b0 = __builtin_amdgcn_permlane32_swap(pk[2].x, pk[3].x, false, false);
+    const auto b1 = __builtin_amdgcn_permlane32_swap(pk[2].y, pk[3].y, false, false);
+    if (ok0) *reinterpret_cast<uint4*>(dst) = make_uint4(a0[0], a1[0], a0[1], a1[1]);
+    if (ok1) *reinterpret_cast<uint4*>(dst + 16) = make_uint4(b0[0], b1[0], b0[1], b1[1]);
 }
 
 // One accumulator value for the epilogue.  With 256 accumulator registers per lane they
@@ -444,20 +440,20 @@ struct RegTiles {
         for (int i = 0; i < 4; ++i) ex[i] += incl - run;
         total = __builtin_amdgcn_readfirstlane(__shfl(incl, 63, 64));
     }
-    // largest expert whose first row tile is <= mt (the table is non-decreasing)
+    // largest expert whose first row tile is <= mt (the table is non-decreasing): a count
+    // over the wave by ballots, no cross-lane data movement
     __device__ __forceinline__ int find(int mt) const {
         const int lane = threadIdx.x & 63;
         int c = 0;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) c += (lane * 4 + i < E && ex[i] <= mt) ? 1 : 0;
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+        for (int i = 0; i < 4; ++i) c += __popcll(__ballot(lane * 4 + i < E && ex[i] <= mt));
         return c - 1;
     }
+    // e is wave-uniform: read it from lane e / 4
     __device__ __forceinline__ int start(int e) const {
         const int q = e & 3;
         const int v = q == 0 ? ex[0] : q == 1 ? ex[1] : q == 2 ? ex[2] : ex[3];
-        return __shfl(v, e >> 2, 64);
+        return __builtin_amdgcn_readlane(v, e >> 2);
     }
 };
 
@@ -800,7 +796,7 @@ void gemm_bf16_lds(GroupedGemm g) {
                     bf16_t* const dst = static_cast<bf16_t*>(g.c) +
                                         (kUp ? ((static_cast<int64_t>(cb) >> 5) * g.rows_max + row) * 32 + 8 * lhi
                                              : row * g.ldc + c0);
-                    store_block_bf16(dst, pk, lhi, row_ok && c0 >= t.n0 && c0 < g.N,
+                    store_block_bf16(dst, pk, row_ok && c0 >= t.n0 && c0 < g.N,
                                      row_ok && c0 + 16 >= t.n0 && c0 + 16 < g.N);
                 } else {
                     // fp32 y_perm (down-projection): groups of 4 columns, N % 4 == 0
@@ -1049,7 +1045,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_up_pairs(GroupedGemm g) {
                 bf16_t* const dst = static_cast<bf16_t*>(g.c) +
                                     ((static_cast<int64_t>(cb) >> 5) * g.rows_max + row) * 32 + 8 * lhi;
                 const bool ok = row_ok && cb >= t.n0 && cb < g.N;  // N, n0, cb: multiples of 32
-                store_block_bf16(dst, pk, lhi, ok, ok);
+                store_block_bf16(dst, pk, ok, ok);
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
@@ -1075,8 +1071,12 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GroupedGemm g) {
     __shared__ __align__(16) float Bs[2][NB][kFBK][kFLD];
 
     const int total = tile_prefix<kFBM>(g.offsets, g.E, tstart);
-    const int mt = blockIdx.x / g.n_tiles;
-    const int nt = blockIdx.x - mt * g.n_tiles;
+    // work item = tile blockIdx / ks, K part blockIdx % ks (ks = 1 unless the down-projection
+    // is split: then part p covers K steps [p nk, (p + 1) nk) and writes fp32 partial sums)
+    const int ks = (EPI == kEpiNone && g.ksplit > 1) ? g.ksplit : 1;
+    const int tile = blockIdx.x / ks, part = blockIdx.x - tile * ks;
+    const int mt = tile / g.n_tiles;
+    const int nt = tile - mt * g.n_tiles;
     if (mt >= total) return;
     const int e = find_expert(tstart, g.E, mt);
     const int64_t row0 = g.offsets[e] + static_cast<int64_t>(mt - tstart[e]) * kFBM;
@@ -1101,8 +1101,10 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GroupedGemm g) {
     struct Regs {
         float4 a[2], b[NB][2];
     };
+    const int nk = (g.K + kFBK - 1) / kFBK / ks;  // K steps of this work item (exact when ks > 1)
+    const int kt0 = part * nk;
     auto gload = [&](Regs& R, int kt) {
-        const int k = kt * kFBK + lk;
+        const int k = (kt0 + kt) * kFBK + lk;
         const bool kv = k < g.K;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
@@ -1143,19 +1145,23 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GroupedGemm g) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
 
-    const int nk = (g.K + kFBK - 1) / kFBK;
     // step kt: MFMAs on LDS buffer kt % 2; register set `next` holds step kt + 1 and goes to
     // the other buffer after them (that buffer was last read before the previous step's
     // barrier), then takes the loads of step kt + 3
+    // a wave whose 32 rows all lie past the segment skips its MFMAs (it still loads and
+    // takes part in the barriers); its block is never stored
+    const bool live = row0 + wm * 32 < row_end;
     auto step = [&](int kt, Regs& next) {
         const int buf = kt & 1;
+        if (live) {
 #pragma unroll
-        for (int ks = 0; ks < kFBK / 2; ++ks) {
-            const float a = As[buf][2 * ks + lhi][wm * 32 + l32];
+            for (int ks = 0; ks < kFBK / 2; ++ks) {
+                const float a = As[buf][2 * ks + lhi][wm * 32 + l32];
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-                acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, Bs[buf][nb][2 * ks + lhi][wn * 32 + l32], acc[nb],
-                                                               0, 0, 0);
+                for (int nb = 0; nb < NB; ++nb)
+                    acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, Bs[buf][nb][2 * ks + lhi][wn * 32 + l32],
+                                                                   acc[nb], 0, 0, 0);
+            }
         }
         if (kt + 1 < nk) sstore(next, buf ^ 1);
         __syncthreads();
@@ -1178,6 +1184,16 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GroupedGemm g) {
     // fixed r the 32 lanes of a half-wave store 32 consecutive columns
     const int n = n0 + wn * 32 + l32;
     if (n >= g.N) return;
+    if (ks > 1) {
+        // a K part: its fp32 sums go to partial[part][row][N], the reduce kernel finishes
+        float* const dst = g.partial + static_cast<int64_t>(part) * g.rows_max * g.N;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int64_t row = row0 + wm * 32 + 8 * (r >> 2) + 4 * lhi + (r & 3);
+            if (row < row_end) dst[row * g.N + n] = acc[0][r];
+        }
+        return;
+    }
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
         int64_t row = row0 + wm * 32 + 8 * (r >> 2) + 4 * lhi + (r & 3);
@@ -1272,7 +1288,7 @@ hipError_t run_bf16(GroupedGemm g, int64_t A_max, hipStream_t s) {
 template <int EPI, bool OB>
 hipError_t run_f32(GroupedGemm g, int64_t A_max, hipStream_t s) {
     g.n_tiles = static_cast<int>(ceil_div(g.N, kFBN));
-    const int64_t blocks = row_tile_bound(A_max, g.E, kFBM) * g.n_tiles;
+    const int64_t blocks = row_tile_bound(A_max, g.E, kFBM) * g.n_tiles * (g.ksplit > 1 ? g.ksplit : 1);
     if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL((gemm_f32<EPI, OB>), dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, s, g);
     return hipGetLastError();
@@ -1342,10 +1358,12 @@ template <int EPI, bool OB>
 hipError_t run_bf16_best(GroupedGemm g, int64_t A_max, hipStream_t s) {
     constexpr bool kUp = EPI != kEpiNone;
     if constexpr (kUp) {
-        // Decode-sized calls (at most 128 rows: a few row tiles) take 128-column tiles, twice
-        // as many workgroups streaming the weights (measured: about 10 us less on a 64-token
-        // top-2 step; no gain from 256 rows up, where the tiles already cover the CUs).
-        if (A_max <= 128 && g.K % 32 == 0) return run_bf16_lds<128, 128, 32, 3, EPI, OB>(g, A_max, s);
+        // Decode-sized calls (at most 128 rows: a few row tiles) take 64 x 128 tiles: twice
+        // the workgroups of 256-column tiles streaming the weights, and half the activation
+        // rows per stage of 128-row tiles, most of which are empty at this size (measured on
+        // a 64-token top-2 step: about 10 us less than 128 x 256, 1.6 us less than 128 x 128;
+        // no gain from 256 rows up, where the tiles already cover the CUs).
+        if (A_max <= 128 && g.K % 32 == 0) return run_bf16_lds<64, 128, 32, 3, EPI, OB>(g, A_max, s);
         // activation rows in 128-byte pieces when K allows it (see gemm_up_pairs)
         if constexpr (OB) {
             if (g.K % 64 == 0) return run_up_pairs<EPI>(g, A_max, s);
@@ -1354,6 +1372,7 @@ hipError_t run_bf16_best(GroupedGemm g, int64_t A_max, hipStream_t s) {
         return run_bf16<EPI, OB, true>(g, A_max, s);
     } else {
         if (g.K % 32 != 0) return hipErrorInvalidValue;  // not reachable through the C ABI (fp % 128 == 0)
+        if (g.ksplit > 1 && A_max <= 128) return run_bf16_lds<64, 256, 32, 3, EPI, OB>(g, A_max, s);
         if (g.ksplit > 1) return run_bf16_lds<128, 256, 32, 3, EPI, OB>(g, A_max, s);
         if (g.N >= 384 && row_tile_bound(A_max, g.E, 128) * ceil_div(g.N, 384) <= device_cus())
             return run_bf16_lds<128, 384, 32, 3, EPI, OB, 4>(g, A_max, s);
@@ -1410,15 +1429,20 @@ hipError_t ffn_pair(const void* x_perm, const int32_t* offsets, int64_t grid_row
         g2.scatter_w = scatter_w;
         g2.c_rows = a_rows;
     }
-    if (!bf16) return y_bf16 ? run_f32<kEpiNone, true>(g2, grid_rows, s) : run_f32<kEpiNone, false>(g2, grid_rows, s);
     // the split is chosen from rows_max (the call's row bound), so a per-expert launch of
     // this call splits like the grouped one
-    g2.ksplit = down_ksplit(rows_max, fp, true);
-    if (g2.ksplit <= 1)
+    g2.ksplit = down_ksplit(rows_max, fp, bf16);
+    if (g2.ksplit <= 1) {
+        if (!bf16) return y_bf16 ? run_f32<kEpiNone, true>(g2, grid_rows, s) : run_f32<kEpiNone, false>(g2, grid_rows, s);
         return y_bf16 ? run_bf16_best<kEpiNone, true>(g2, grid_rows, s) : run_bf16_best<kEpiNone, false>(g2, grid_rows, s);
+    }
     // partial tiles after H in the workspace: ksplit x rows_max x h fp32
-    g2.partial = reinterpret_cast<float*>(static_cast<unsigned char*>(hbuf) + round_up(rows_max * fp * 2, 256));
-    err = y_bf16 ? run_bf16_best<kEpiNone, true>(g2, grid_rows, s) : run_bf16_best<kEpiNone, false>(g2, grid_rows, s);
+    g2.partial = reinterpret_cast<float*>(static_cast<unsigned char*>(hbuf) +
+                                          round_up(rows_max * fp * (bf16 ? 2 : 4), 256));
+    if (bf16)
+        err = y_bf16 ? run_bf16_best<kEpiNone, true>(g2, grid_rows, s) : run_bf16_best<kEpiNone, false>(g2, grid_rows, s);
+    else
+        err = run_f32<kEpiNone, false>(g2, grid_rows, s);  // partial tiles only
     if (err != hipSuccess) return err;
     const int64_t n4 = grid_rows * (h / 4);
     const int blocks = static_cast<int>(std::min<int64_t>(ceil_div(n4, 256), 8LL * device_cus()));

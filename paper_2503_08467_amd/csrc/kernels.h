@@ -11,15 +11,18 @@ namespace moe {
 constexpr int kInnerAlign = 128;  // packed inner width is a multiple of this
 constexpr int kDispatchChunk = 1024;  // assignments per dispatch workgroup
 
-// K parts of the bf16 down-projection.  A call with few rows has few row tiles, each with a
-// long K loop, and leaves most CUs idle; splitting K spreads the weight reads over more
-// workgroups (fp32 partial tiles, summed in a fixed order afterwards).  A function of the
-// call's sizes only (the row bound, not the routing), so every launch path of one call
-// shape rounds the same way.  fp is the packed inner width (a multiple of kInnerAlign).
+// K parts of the down-projection.  A call with few rows has few row tiles, each with a long
+// K loop, and leaves most CUs idle; splitting K spreads the weight reads over more workgroups
+// (fp32 partial tiles, summed in a fixed order afterwards).  A function of the call's sizes
+// only (the row bound, not the routing), so every launch path of one call shape rounds the
+// same way.  fp is the packed inner width (a multiple of kInnerAlign).
+//   bf16: up to 8 parts for at most 512 rows (measured: no gain from 1024 rows up);
+//   fp32: 4 parts for at most 1024 rows (its 64 x 64 tiles have a K loop twice as slow).
 inline int down_ksplit(int64_t A_max, int64_t fp, bool bf16) {
-    if (!bf16 || A_max > 512) return 1;  // measured: no gain from 1024 rows up
-    int s = A_max <= 256 ? 8 : 4;
     const int64_t nk = fp / 32;  // K steps of 32
+    if (!bf16) return (A_max <= 1024 && nk % 4 == 0 && nk / 4 >= 8) ? 4 : 1;
+    if (A_max > 512) return 1;
+    int s = A_max <= 256 ? 8 : 4;
     while (s > 1 && (nk % s != 0 || nk / s < 8)) s >>= 1;
     return s;
 }
@@ -27,10 +30,10 @@ inline int down_ksplit(int64_t A_max, int64_t fp, bool bf16) {
 // Bytes of fp32 partial tiles to reserve past the H buffer for a call bound of A_max rows:
 // the most that any call with at most A_max rows needs (down_ksplit * rows * h * 4), so
 // that a workspace sized for a bound also serves every smaller call.  The product is
-// largest at the ends of the two split ranges (256 and 512 rows).
+// largest at the ends of the split ranges (256, 512 and 1024 rows).
 inline size_t down_partial_bytes(int64_t A_max, int64_t h, int64_t fp, bool bf16) {
     int64_t most = 0;
-    for (int64_t end : {int64_t(256), int64_t(512)}) {
+    for (int64_t end : {int64_t(256), int64_t(512), int64_t(1024)}) {
         const int64_t a = A_max < end ? A_max : end;
         const int64_t s = down_ksplit(a, fp, bf16);
         if (s > 1 && s * a > most) most = s * a;

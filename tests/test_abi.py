@@ -106,7 +106,8 @@ def test_sizes_follow_the_padded_layout(lib):
 
 
 def test_ffn_workspace_holds_split_partials(lib):
-    """Small bf16 calls split the second product's K: fp32 partials of S x A_max x h follow H."""
+    """Small calls split the second product's K: fp32 partials of S x A_max x h follow H
+    (bf16: up to 8 parts up to 512 rows; fp32: 4 parts up to 1024 rows)."""
     al = lambda v: (v + 255) // 256 * 256
     ws = lambda A, h, f, dt=_lib.MOE_BF16: lib.moe_ffn_workspace_size(A, 64, h, f, _lib.MOE_ACT_GELU, dt)
     # decode-sized: 128 rows, fp = 4096 (128 K steps of 32) -> 8 parts
@@ -118,12 +119,16 @@ def test_ffn_workspace_holds_split_partials(lib):
     # short K: fp = 128 has 4 steps, too few to split
     assert ws(128, 1024, 128) == al(128 * 128 * 2) + 256
     # larger calls do not split but keep the room (a workspace sized for a bound serves
-    # every smaller call); fp32 never splits
+    # every smaller call)
     assert ws(513, 768, 3072) == al(513 * 3072 * 2) + al(2048 * 768 * 4) + 256
-    assert ws(128, 1024, 4096, _lib.MOE_F32) == al(128 * 4096 * 4) + 256
-    for h, f in [(1024, 4096), (4096, 1792), (768, 3072), (64, 128), (72, 1000)]:
-        sizes = [ws(a, h, f) for a in range(0, 1100, 7)]
-        assert sizes == sorted(sizes), (h, f)
+    assert ws(128, 1024, 4096, _lib.MOE_F32) == al(128 * 4096 * 4) + al(4 * 128 * 1024 * 4) + 256
+    assert ws(1025, 768, 3072, _lib.MOE_F32) == al(1025 * 3072 * 4) + al(4 * 1024 * 768 * 4) + 256
+    # fp32 with fp = 512: 16 K steps, 4 parts would leave 4 each -> no split
+    assert ws(128, 1024, 512, _lib.MOE_F32) == al(128 * 512 * 4) + 256
+    for dt in (_lib.MOE_BF16, _lib.MOE_F32):
+        for h, f in [(1024, 4096), (4096, 1792), (768, 3072), (64, 128), (72, 1000)]:
+            sizes = [ws(a, h, f, dt) for a in range(0, 1300, 7)]
+            assert sizes == sorted(sizes), (h, f, dt)
 
 
 def test_ffn_and_combine_reject_bad_arguments(lib):

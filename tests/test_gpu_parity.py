@@ -61,7 +61,13 @@ def test_route_parity_on_workloads(name, T):
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("T,h,E,k", [(1, 8, 1, 1), (17, 72, 3, 2), (100, 256, 16, 16), (65, 136, 17, 4),
                                      (130, 64, 64, 2), (33, 512, 200, 8), (64, 96, 256, 3), (257, 1024, 128, 1),
-                                     (16449, 64, 136, 2)])  # more 64-token workgroups than CUs
+                                     (16449, 64, 136, 2),  # more 64-token workgroups than CUs
+                                     # the persistent kernel (h % 256 == 0, E % 8 == 0, E <= 128, k <= 8):
+                                     # several tiles per workgroup, partial last tiles, one to sixteen
+                                     # chunks per row, one to four 32-expert blocks
+                                     (1000, 768, 64, 2), (70, 4096, 8, 2), (5000, 1024, 64, 8), (33, 512, 16, 3),
+                                     (9000, 2048, 40, 4), (20000, 256, 24, 2), (300, 1536, 96, 5),
+                                     (70000, 256, 32, 2)])  # more than 8 tiles per workgroup
 @pytest.mark.parametrize("bias_kind", ["none", "row", "shared"])
 def test_route_shapes_and_bias(dtype, T, h, E, k, bias_kind):
     rng = np.random.default_rng(T * 1000 + E)
@@ -142,15 +148,30 @@ def _check_dispatch(idx, E, h=64, dtype=torch.bfloat16):
 
 
 # up to 16384 assignments one fused kernel dispatches, above it three kernels: both sides of
-# that boundary are covered (8192 x 2, 16384 x 1 fused; 16385 x 1 and larger not)
+# that boundary are covered (8192 x 2, 16384 x 1 fused; 16385 x 1 and larger not), as are
+# chunk edges and large skewed batches
 @pytest.mark.parametrize("T,k,E", [(0, 1, 8), (1, 1, 1), (5, 2, 5), (1000, 1, 64), (1023, 2, 7), (1024, 2, 256),
                                    (3000, 3, 100), (8192, 2, 3), (16384, 1, 128), (16385, 1, 64), (32768, 2, 64),
-                                   (4096, 8, 256)])
+                                   (4096, 8, 256), (4097, 1, 2), (131072, 2, 64), (131073, 2, 64),
+                                   (70000, 4, 256)])
 def test_dispatch_bit_exact(T, k, E):
     rng = np.random.default_rng(T + 7 * E)
     p = rng.dirichlet(np.full(E, 0.3))  # skewed popularity, many empty experts
-    idx = np.stack([rng.choice(E, size=k, replace=False, p=p) for _ in range(T)]).astype(np.int32) \
-        if T else np.zeros((0, k), np.int32)
+    # k distinct ids per token drawn without replacement with probabilities p (Gumbel top-k)
+    keys = np.log(np.maximum(p, 1e-300))[None, :] - np.log(-np.log(rng.random((T, E))))
+    idx = np.argsort(-keys, axis=1, kind="stable")[:, :k].astype(np.int32)
+    _check_dispatch(idx, E)
+
+
+def test_dispatch_fused_skew_and_invalid_ids():
+    """95 % of the assignments on one expert and some ids invalid, over many dispatch
+    chunks: counts and ranks stay exact."""
+    rng = np.random.default_rng(11)
+    T, k, E = 30000, 2, 64
+    idx = np.where(rng.random((T, k)) < 0.95, 17, rng.integers(0, E, (T, k))).astype(np.int32)
+    idx[:, 1] = np.where(idx[:, 1] == idx[:, 0], (idx[:, 0] + 1) % E, idx[:, 1])
+    idx[::97, 0] = -5
+    idx[::89, 1] = E + 2
     _check_dispatch(idx, E)
 
 
