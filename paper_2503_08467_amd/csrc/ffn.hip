@@ -18,8 +18,9 @@
 // in fp32, rounds once, and stores 8-byte vectors straight from the accumulators (into
 // K-blocked H for GEMM1).  Calls of at most 512 rows split GEMM2's K into parts summed by
 // split_reduce in a fixed order.
-// fp32 path (gemm_f32): 64 x 64 tiles on v_mfma_f32_32x32x2_f32, row-major operands staged
-// through two LDS buffers from registers.
+// fp32 path (gemm_f32_lds): 32 x 128 tiles on v_mfma_f32_32x32x2_f32, row-major operands in
+// 128-byte row pieces through three direct-to-LDS stages; gemm_f32 (register-staged 64 x 64
+// tiles) only for an up-projection whose h is not a multiple of 32.
 #include "common.h"
 #include "kernels.h"
 #include "lds_dma.h"
@@ -1210,6 +1211,207 @@ __global__ __launch_bounds__(kThreads) void gemm_f32(GroupedGemm g) {
     }
 }
 
+// ------------------------------------------------------------------ fp32 pipelined kernel
+//
+// fp32 operands whose K is a multiple of 32 (every down-projection; the up-projection when
+// h % 32 == 0).  Tiles of 32 activation rows x 128 weight rows of each matrix; four waves,
+// wave w owning output columns 32 w .. 32 w + 31 of the tile in every matrix.
+// v_mfma_f32_32x32x2_f32 takes the weights as its first operand, so a lane ends up holding
+// one activation row and, in each group of four registers, four consecutive output columns.
+// K advances 32 values (128 bytes of every row) per stage; a stage goes straight to LDS as
+// 1 KiB direct loads of 8 rows x 128 bytes, NS stages with NS - 1 in flight across K steps
+// and work items (the bf16 kernel's pipeline).  Inside a stage a lane reads, for each group
+// of 8 K values, 4 consecutive K values of its row as one 16-byte fragment and feeds element
+// c to the c-th of four MFMAs; the other half-wave supplies the group's other 4 K values, so
+// the four MFMAs together sum over the whole group.  32-row tiles hold at least one valid
+// row each, and an expert's rows waste at most 31 padded rows.  Persistent grid: work items
+// (tile, K part) are dealt to the XCDs in contiguous runs and round-robin to each XCD's
+// workgroups.
+constexpr int kF2BM = 32, kF2BN = 128, kF2BK = 32;  // kF2BK counts floats: 128-byte row pieces
+
+template <int NB>
+struct F32Shape {
+    static constexpr int kRows = kF2BM + NB * kF2BN;  // LDS rows per stage
+    static constexpr int kStageBytes = kRows * kF2BK * 4;
+    static constexpr int kLPW = kRows / 8 / 4;         // 1 KiB loads per wave per stage
+    static constexpr int kStages = NB == 1 ? 3 : 2;    // two workgroups per CU either way
+    static constexpr size_t kBytes = static_cast<size_t>(kStages) * kStageBytes;
+};
+
+template <int EPI, bool OB>
+__global__ __launch_bounds__(kThreads, 2) void gemm_f32_lds(GroupedGemm g) {
+    constexpr int NB = (EPI == kEpiSwiglu) ? 2 : 1;
+    typedef F32Shape<NB> S;
+    constexpr int BM = kF2BM, BN = kF2BN, LPW = S::kLPW, NS = S::kStages;
+    constexpr int kStageBytes = S::kStageBytes;
+    constexpr bool kUp = EPI != kEpiNone;
+    static_assert(LPW == 1 + 4 * NB, "load 0 carries the 32 activation rows, loads 4 nb + 1 .. 4 nb + 4 matrix nb");
+    __shared__ int tstart[kThreads + 1];
+    extern __shared__ __align__(1024) unsigned char smem_raw[];
+
+    const int total_m = tile_prefix<BM>(g.offsets, g.E, tstart);
+    const LdsTiles tiles{tstart, g.E};
+    // work item L: tile L / ks, K part L % ks (ks = 1 unless the down-projection is split)
+    const int ks = (!kUp && g.ksplit > 1) ? g.ksplit : 1;
+    const int total = total_m * g.n_tiles * ks;
+    const int per = (total + 7) >> 3;
+    const int xcd = blockIdx.x & 7, nslot = gridDim.x >> 3;
+    const int t_first = xcd * per + static_cast<int>(blockIdx.x >> 3);
+    const int t_end = min(total, xcd * per + per);
+    if (t_first >= t_end) return;
+    const int nk = g.K / kF2BK / ks;  // stages per work item
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint32_t lds0 = lds_address(smem_raw);
+
+    // Per-lane byte offsets of this wave's loads: load j fills LDS rows 8 (4 j + wave) + lane
+    // / 8 of a stage, 16-byte slot lane % 8, from global slot (lane % 8) ^ swz(row).  Rows past
+    // a buffer smaller than one tile repeat its last row.
+    const int r_lane = lane >> 3;
+    const int a_lim = static_cast<int>(g.rows_max < BM ? g.rows_max : BM) - 1;
+    const int b_lim = (g.N < BN ? g.N : BN) - 1;
+    uint32_t voff[LPW];
+#pragma unroll
+    for (int j = 1; j < LPW; ++j) {
+        const int R = 8 * (4 * j + wave) + r_lane;
+        const int kc = (lane & 7) ^ ((R >> 1) & 7);
+        const int r = min((R - BM) % BN, b_lim);
+        voff[j] = static_cast<uint32_t>(r) * static_cast<uint32_t>(4 * g.K) + static_cast<uint32_t>(kc * 16);
+    }
+    const int ra = min(8 * wave + r_lane, a_lim);  // this lane's activation row in load 0
+    const uint32_t kca = static_cast<uint32_t>(((lane & 7) ^ (((8 * wave + r_lane) >> 1) & 7)) * 16);
+
+    // ---- load cursor: work item li, K step lk, scalar bases of the item's rows
+    int li = t_first, lk = 0;
+    const unsigned char *src_a = nullptr, *src_b0 = nullptr, *src_b1 = nullptr;
+    auto set_item = [&](int L) {
+        const TileGeom t = tile_geom<BM, BN>(g, tiles, total_m, L / ks);
+        const int64_t k0 = static_cast<int64_t>(L % ks) * nk * kF2BK;  // first K value of the item
+        if (g.gather) {
+            // absolute source row (T h 4 < 4 GiB is checked by the host)
+            const int64_t src = source_row(g, t.row_base + ra);
+            voff[0] = static_cast<uint32_t>(src) * static_cast<uint32_t>(4 * g.K) + kca;
+            src_a = uniform_ptr(static_cast<const float*>(g.a) + k0);
+        } else {
+            voff[0] = static_cast<uint32_t>(ra) * static_cast<uint32_t>(4 * g.K) + kca;
+            src_a = uniform_ptr(static_cast<const float*>(g.a) + t.row_base * g.K + k0);
+        }
+        const int64_t boff = t.e * g.b_estride + static_cast<int64_t>(t.n_base) * g.K + k0;
+        src_b0 = uniform_ptr(static_cast<const float*>(g.b) + boff);
+        src_b1 = NB > 1 ? uniform_ptr(static_cast<const float*>(g.b2) + boff) : src_b0;
+    };
+    int issued = 0;  // stages issued by this wave so far
+    auto issue_next = [&]() {
+        if (li >= t_end) return;
+        const uint32_t dst = lds0 + (issued % NS) * kStageBytes;
+        const int kb = lk * kF2BK * 4;  // bytes into every row
+#pragma unroll
+        for (int j = 0; j < LPW; ++j) {
+            const unsigned char* base = j == 0 ? src_a : ((j - 1) / 4 == 0 ? src_b0 : src_b1);
+            load_lds16(base + kb, voff[j], dst + (4 * j + wave) * 1024);
+        }
+        ++issued;
+        if (++lk == nk) {
+            lk = 0;
+            li += nslot;
+            if (li < t_end) set_item(li);
+        }
+    };
+    set_item(li);
+#pragma unroll
+    for (int st = 0; st < NS - 1; ++st) issue_next();
+
+    const int l32 = lane & 31, lhi = lane >> 5;
+    int consumed = 0;
+    for (int L = t_first; L < t_end; L += nslot) {
+        const TileGeom t = tile_geom<BM, BN>(g, tiles, total_m, L / ks);
+        f32x16_t acc[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
+
+        // publish the item's first stage (after an epilogue its stores share the counter)
+        wait_lgkm0();
+        if (L != t_first) wait_vmcnt<0>();
+        else wait_stages<LPW, NS>(issued - consumed - 1);
+        stage_barrier();
+        issue_next();
+        for (int ck = 0; ck < nk; ++ck) {
+            const unsigned char* st = smem_raw + (consumed % NS) * kStageBytes;
+#pragma unroll
+            for (int q = 0; q < kF2BK / 8; ++q) {
+                const int slot = 2 * q + lhi;
+                const float4 xf = *reinterpret_cast<const float4*>(st + l32 * 128 + ((slot ^ ((l32 >> 1) & 7)) << 4));
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) {
+                    const int Rw = BM + nb * BN + 32 * wave + l32;
+                    const float4 wf =
+                        *reinterpret_cast<const float4*>(st + Rw * 128 + ((slot ^ ((Rw >> 1) & 7)) << 4));
+                    acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(wf.x, xf.x, acc[nb], 0, 0, 0);
+                    acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(wf.y, xf.y, acc[nb], 0, 0, 0);
+                    acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(wf.z, xf.z, acc[nb], 0, 0, 0);
+                    acc[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(wf.w, xf.w, acc[nb], 0, 0, 0);
+                }
+            }
+            ++consumed;
+            if (ck + 1 < nk) {
+                // publish the next stage: own reads of this one done, own loads of the next
+                // landed; then refill this stage's buffer
+                wait_lgkm0();
+                wait_stages<LPW, NS>(issued - consumed - 1);
+                stage_barrier();
+                issue_next();
+            }
+        }
+
+        // ---- epilogue.  Lane: activation row row_base + l32; register 4 q + c: output column
+        // n_base + 32 wave + 8 q + 4 lhi + c.
+        const int64_t row = t.row_base + l32;
+        const int64_t row_lo = t.row0 > 0 ? t.row0 : 0;
+        const bool row_ok = row >= row_lo && row < t.row_end;
+        const int cb = t.n_base + 32 * wave + 4 * lhi;
+        if (ks > 1) {
+            // a K part: its fp32 sums go to partial[part][row][N], the reduce kernel finishes
+            float* const dst = g.partial + static_cast<int64_t>(L % ks) * g.rows_max * g.N;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int col = cb + 8 * q;
+                if (row_ok && col >= t.n0 && col < g.N)
+                    *reinterpret_cast<float4*>(dst + row * g.N + col) =
+                        make_float4(acc[0][4 * q], acc[0][4 * q + 1], acc[0][4 * q + 2], acc[0][4 * q + 3]);
+            }
+            continue;
+        }
+        int64_t orow = row;
+        float scale = 1.f;
+        if (!kUp && g.scatter) {
+            // the grouped row's token and gate weight
+            const int64_t src = row_ok ? g.scatter[row] : 0;
+            orow = src < 0 ? 0 : (src >= g.c_rows ? g.c_rows - 1 : src);
+            scale = row_ok ? g.scatter_w[orow] : 0.f;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int col = cb + 8 * q;
+            if (!row_ok || col < t.n0 || col >= g.N) continue;
+            float v[4];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) v[c] = scale * epilogue<EPI>(acc[0][4 * q + c], acc[NB - 1][4 * q + c]);
+            if constexpr (OB) {
+                uint2 pk;
+                pk.x = pack_bf16x2(v[0], v[1]);
+                pk.y = pack_bf16x2(v[2], v[3]);
+                *reinterpret_cast<uint2*>(static_cast<bf16_t*>(g.c) + orow * g.ldc + col) = pk;
+            } else {
+                *reinterpret_cast<float4*>(static_cast<float*>(g.c) + orow * g.ldc + col) =
+                    make_float4(v[0], v[1], v[2], v[3]);
+            }
+        }
+    }
+}
+
 // ------------------------------------------------------------------ split-K reduce
 //
 // out[p] = sum over s of partial[s][p] (s ascending) for the grouped rows p of the call,
@@ -1285,8 +1487,27 @@ hipError_t run_bf16(GroupedGemm g, int64_t A_max, hipStream_t s) {
     return hipGetLastError();
 }
 
+int device_cus();
+
+template <int EPI, bool OB>
+hipError_t run_f32_lds(GroupedGemm g, int64_t A_max, hipStream_t s) {
+    constexpr size_t lds = F32Shape<(EPI == kEpiSwiglu) ? 2 : 1>::kBytes;
+    static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_f32_lds<EPI, OB>),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                       static_cast<int>(lds));
+    if (attr != hipSuccess) return attr;
+    g.n_tiles = static_cast<int>(ceil_div(g.N, kF2BN));
+    const int64_t items = row_tile_bound(A_max, g.E, kF2BM) * g.n_tiles * (g.ksplit > 1 ? g.ksplit : 1);
+    if (items == 0) return hipSuccess;
+    // persistent grid: at most two workgroups per CU, a multiple of the 8 XCDs
+    const int64_t blocks = round_up(std::min<int64_t>(items, 2 * static_cast<int64_t>(device_cus())), 8);
+    hipLaunchKernelGGL((gemm_f32_lds<EPI, OB>), dim3(static_cast<unsigned>(blocks)), dim3(kThreads), lds, s, g);
+    return hipGetLastError();
+}
+
 template <int EPI, bool OB>
 hipError_t run_f32(GroupedGemm g, int64_t A_max, hipStream_t s) {
+    if (g.K % kF2BK == 0) return run_f32_lds<EPI, OB>(g, A_max, s);
     g.n_tiles = static_cast<int>(ceil_div(g.N, kFBN));
     const int64_t blocks = row_tile_bound(A_max, g.E, kFBM) * g.n_tiles * (g.ksplit > 1 ? g.ksplit : 1);
     if (blocks == 0) return hipSuccess;

@@ -17,7 +17,7 @@ constexpr int kDispatchChunk = 1024;  // assignments per dispatch workgroup
 // only (the row bound, not the routing), so every launch path of one call shape rounds the
 // same way.  fp is the packed inner width (a multiple of kInnerAlign).
 //   bf16: up to 8 parts for at most 512 rows (measured: no gain from 1024 rows up);
-//   fp32: 4 parts for at most 1024 rows (its 64 x 64 tiles have a K loop twice as slow).
+//   fp32: 4 parts for at most 1024 rows (its K loop is four times as slow as bf16's).
 inline int down_ksplit(int64_t A_max, int64_t fp, bool bf16) {
     const int64_t nk = fp / 32;  // K steps of 32
     if (!bf16) return (A_max <= 1024 && nk % 4 == 0 && nk / 4 >= 8) ? 4 : 1;
