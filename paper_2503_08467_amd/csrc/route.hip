@@ -56,6 +56,200 @@ struct GateFrag<float> {
 };
 
 constexpr int kWaves = 4;
+constexpr int kNoExpert = 0x7fffffff;
+constexpr int kRegPicks = 8;  // picks kept in registers (one per lane of a token's group)
+
+// A token's picks as held by one lane of its group: pick q of the token (lane q), and the
+// sum of the k pick weights.
+struct Picks {
+    int e;
+    float p, wsum;
+};
+
+// Step 1's selection for one token, eight lanes per token: lane q of the group holds NV
+// logits lv[] (-inf for padding) and selection scores sv[] = logit + bias for experts
+// M::ex(q, j).  Softmax over the logits, then k rounds of arg-max over the scores in which
+// the lower expert id wins ties (each lane scans its experts upward with a strict
+// comparison, and the lane reduction prefers the lower id on ties); the weight of a pick is
+// the softmax of its logit.  With k <= kRegPicks lane q keeps pick q and the caller stores
+// it (store_pick) once every token of the workgroup is done, so no store waits on another;
+// a larger k writes each pick as it is found and renormalises through memory afterwards.
+template <int NV, typename M>
+__device__ __forceinline__ Picks select_token(const float (&lv)[NV], const float (&sv)[NV], int q, int E, int k,
+                                              int renorm, bool live, int64_t t, int32_t* __restrict__ idx,
+                                              float* __restrict__ w) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) mx = fmaxf(mx, lv[j]);
+#pragma unroll
+    for (int o = 1; o < 8; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+    float den = 0.f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) den += (M::ex(q, j) < E) ? expf(lv[j] - mx) : 0.f;
+#pragma unroll
+    for (int o = 1; o < 8; o <<= 1) den += __shfl_xor(den, o, kWave);
+
+    Picks r{-1, 0.f, 0.f};
+    uint32_t taken = 0;
+    float wsum = 0.f;
+    for (int j = 0; j < k; ++j) {
+        float bs = -INFINITY, bl = -INFINITY;
+        int be = kNoExpert;
+#pragma unroll
+        for (int jj = 0; jj < NV; ++jj) {
+            const int e = M::ex(q, jj);
+            if (e < E && !((taken >> jj) & 1u) && (sv[jj] > bs || be == kNoExpert)) {
+                bs = sv[jj];
+                bl = lv[jj];
+                be = e;
+            }
+        }
+#pragma unroll
+        for (int o = 1; o < 8; o <<= 1) {
+            const float os = __shfl_xor(bs, o, kWave);
+            const float ol = __shfl_xor(bl, o, kWave);
+            const int oe = __shfl_xor(be, o, kWave);
+            if (oe != kNoExpert && (be == kNoExpert || os > bs || (os == bs && oe < be))) {
+                bs = os;
+                bl = ol;
+                be = oe;
+            }
+        }
+        const bool found = be != kNoExpert;
+        if (found && M::owner(be) == q) taken |= 1u << M::slot(be);
+        const float p = found ? expf(bl - mx) / den : 0.f;
+        wsum += p;
+        if (j == q) {
+            r.e = found ? be : -1;
+            r.p = p;
+        }
+        if (k > kRegPicks && q == 0 && live) {
+            idx[t * k + j] = found ? be : -1;
+            w[t * k + j] = p;
+        }
+    }
+    r.wsum = wsum;
+    if (k > kRegPicks && renorm && q == 0 && live)
+        for (int j = 0; j < k; ++j) w[t * k + j] = w[t * k + j] / wsum;
+    return r;
+}
+
+// Lane q's pick of its token (k <= kRegPicks): idx[t k + q], w[t k + q], renormalised over
+// the k picks on request.
+__device__ __forceinline__ void store_pick(const Picks& r, int q, int k, int renorm, bool live, int64_t t,
+                                           int32_t* __restrict__ idx, float* __restrict__ w) {
+    if (k <= kRegPicks && live && q < k) {
+        idx[t * k + q] = r.e;
+        w[t * k + q] = renorm ? r.p / r.wsum : r.p;
+    }
+}
+
+// Lane exchanges inside a quad (four consecutive lanes) as DPP operand moves: a VALU
+// instruction each, no LDS round trip.
+constexpr int kDppXor1 = 0xB1;  // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;  // quad_perm [2, 3, 0, 1]
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+    return __int_as_float(dpp_i<CTRL>(__float_as_int(v)));
+}
+
+// Arg-max step between quad partners: the higher score, the lower expert id on ties, a
+// lane without a candidate (kNoExpert) losing to any other.  Symmetric, so both partners
+// end with the same winner.
+template <int CTRL>
+__device__ __forceinline__ void quad_best(float& bs, float& bl, int& be) {
+    const float os = dpp_f<CTRL>(bs);
+    const float ol = dpp_f<CTRL>(bl);
+    const int oe = dpp_i<CTRL>(be);
+    const bool other = oe != kNoExpert && (be == kNoExpert || os > bs || (os == bs && oe < be));
+    bs = other ? os : bs;
+    bl = other ? ol : bl;
+    be = other ? oe : be;
+}
+
+constexpr int kQuadPicks = 8;  // picks kept in registers with four lanes per token (two each)
+
+struct QuadPicks {
+    int e0, e1;  // picks q and q + 4 of the token
+    float p0, p1, wsum;
+};
+
+// Step 1's selection with four lanes per token (a quad): lane q holds the logits lv[] and
+// selection scores sv[] = logit + bias of experts NV q .. NV q + NV - 1 (sv = -inf for
+// padding, whose lv is never used).  Every choice below is a select, not a branch: a
+// branch around each element would serialise the LDS reads and exponentials.  Softmax
+// over the logits (exponentials in base 2: e^(l - m) = 2^((l - m) log2 e)), then k rounds of
+// arg-max over the scores in which the lower expert id wins ties; a pick's weight is the
+// softmax of its logit.  Lane q keeps picks q and q + 4; with k > kQuadPicks every pick is
+// written as it is found and renormalised through memory afterwards.
+template <int NV>
+__device__ __forceinline__ QuadPicks select_quad(const float (&lv)[NV], const float (&sv)[NV], int q, int E, int k,
+                                                 int renorm, bool live, int64_t t, int32_t* __restrict__ idx,
+                                                 float* __restrict__ w) {
+    constexpr float kLog2e = 1.4426950408889634f;
+    const int e0 = NV * q;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) mx = fmaxf(mx, lv[j]);
+    mx = fmaxf(mx, dpp_f<kDppXor1>(mx));
+    mx = fmaxf(mx, dpp_f<kDppXor2>(mx));
+    float den = 0.f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        const float x = __builtin_amdgcn_exp2f((lv[j] - mx) * kLog2e);
+        den += e0 + j < E ? x : 0.f;
+    }
+    den += dpp_f<kDppXor1>(den);
+    den += dpp_f<kDppXor2>(den);
+
+    QuadPicks r{-1, -1, 0.f, 0.f, 0.f};
+    uint64_t taken = 0;
+    float wsum = 0.f;
+    for (int j = 0; j < k; ++j) {
+        float bs = -INFINITY, bl = -INFINITY;
+        int be = kNoExpert;
+#pragma unroll
+        for (int jj = 0; jj < NV; ++jj) {
+            const bool take = e0 + jj < E && !((taken >> jj) & 1u) && (sv[jj] > bs || be == kNoExpert);
+            bs = take ? sv[jj] : bs;
+            bl = take ? lv[jj] : bl;
+            be = take ? e0 + jj : be;
+        }
+        quad_best<kDppXor1>(bs, bl, be);
+        quad_best<kDppXor2>(bs, bl, be);
+        const bool found = be != kNoExpert;
+        const int rel = be - e0;
+        taken |= (found && rel >= 0 && rel < NV) ? (1ull << rel) : 0ull;
+        const float p = found ? __builtin_amdgcn_exp2f((bl - mx) * kLog2e) / den : 0.f;
+        wsum += p;
+        const int pe = found ? be : -1;
+        r.e0 = j == q ? pe : r.e0;
+        r.p0 = j == q ? p : r.p0;
+        r.e1 = j == q + 4 ? pe : r.e1;
+        r.p1 = j == q + 4 ? p : r.p1;
+        if (k > kQuadPicks && q == 0 && live) {
+            idx[t * k + j] = pe;
+            w[t * k + j] = p;
+        }
+    }
+    r.wsum = wsum;
+    if (k > kQuadPicks && renorm && q == 0 && live)
+        for (int j = 0; j < k; ++j) w[t * k + j] = w[t * k + j] / wsum;
+    return r;
+}
+
+// Expert of lane q's j-th logit: experts q, q + 8, q + 16, ...; owner and slot invert it.
+template <int NV>
+struct StridedExperts {
+    static __device__ __forceinline__ int ex(int q, int j) { return q + 8 * j; }
+    static __device__ __forceinline__ int owner(int e) { return e & 7; }
+    static __device__ __forceinline__ int slot(int e) { return e >> 3; }
+};
 
 template <int NB>
 constexpr int route_ldw() { return NB * 32 + 8; }  // padded row: 8 token rows hit 8 bank groups
@@ -111,7 +305,6 @@ __global__ __launch_bounds__(kWaves * kWave) void route_kernel(const Tin* __rest
     const int tt = wave * 8 + (lane >> 3), q = lane & 7;
     const int64_t t = tok0 + tt;
     float lv[NV], sv[NV];
-    float mx = -INFINITY;
 #pragma unroll
     for (int j = 0; j < NV; ++j) {
         const int e = q + 8 * j;
@@ -120,52 +313,9 @@ __global__ __launch_bounds__(kWaves * kWave) void route_kernel(const Tin* __rest
         const bool ok = e < E;
         lv[j] = ok ? v : -INFINITY;
         sv[j] = ok ? ((bias && t < T) ? v + bias[t * bias_stride + e] : v) : -INFINITY;
-        mx = fmaxf(mx, lv[j]);
     }
-#pragma unroll
-    for (int o = 1; o < 8; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
-    float den = 0.f;
-#pragma unroll
-    for (int j = 0; j < NV; ++j) den += (q + 8 * j < E) ? expf(lv[j] - mx) : 0.f;
-#pragma unroll
-    for (int o = 1; o < 8; o <<= 1) den += __shfl_xor(den, o, kWave);
-
-    uint32_t taken = 0;
-    float wsum = 0.f;
-    for (int j = 0; j < k; ++j) {
-        float bs = -INFINITY, bl = -INFINITY;
-        int be = 0x7fffffff;
-#pragma unroll
-        for (int jj = 0; jj < NV; ++jj) {
-            const int e = q + 8 * jj;
-            if (e < E && !((taken >> jj) & 1u) && (sv[jj] > bs || be == 0x7fffffff)) {
-                bs = sv[jj];
-                bl = lv[jj];
-                be = e;
-            }
-        }
-#pragma unroll
-        for (int o = 1; o < 8; o <<= 1) {
-            const float os = __shfl_xor(bs, o, kWave);
-            const float ol = __shfl_xor(bl, o, kWave);
-            const int oe = __shfl_xor(be, o, kWave);
-            if (oe != 0x7fffffff && (be == 0x7fffffff || os > bs || (os == bs && oe < be))) {
-                bs = os;
-                bl = ol;
-                be = oe;
-            }
-        }
-        const bool found = be != 0x7fffffff;
-        if (found && (be & 7) == q) taken |= 1u << (be >> 3);
-        const float p = found ? expf(bl - mx) / den : 0.f;
-        wsum += p;
-        if (q == 0 && t < T) {
-            idx[t * k + j] = found ? be : -1;
-            w[t * k + j] = p;
-        }
-    }
-    if (renorm && q == 0 && t < T)
-        for (int j = 0; j < k; ++j) w[t * k + j] = w[t * k + j] / wsum;
+    const Picks pk = select_token<NV, StridedExperts<NV>>(lv, sv, q, E, k, renorm, t < T, t, idx, w);
+    store_pick(pk, q, k, renorm, t < T, t, idx, w);
 }
 
 // ---------------------------------------------------------------- bf16, h % 64 == 0, E > 32
@@ -197,7 +347,7 @@ struct RouteLds {
     static constexpr size_t kBytes = kStageBytes > kLogitBytes ? kStageBytes : kLogitBytes;
 };
 
-template <int NBW>
+template <int NBW, int BIAS>
 __global__ __launch_bounds__(kWaves * kWave) void route_lds_kernel(const bf16_t* __restrict__ x,
                                                                    const bf16_t* __restrict__ wg, int64_t T,
                                                                    int h, int E, int k,
@@ -245,29 +395,36 @@ __global__ __launch_bounds__(kWaves * kWave) void route_lds_kernel(const bf16_t*
     for (int st = 0; st < NS - 1; ++st)
         if (issued < nk) issue();
 
-    // Each epilogue lane owns NV consecutive experts of one token (two passes of 32 tokens).
-    // The selection bias of those tokens is fetched now, in contiguous runs per lane, so
-    // that its latency hides behind the K loop.
-    constexpr int NV = EP / 8;
-    const int q = lane & 7;
-    float bv[2][NV];
+    // Each epilogue lane owns NV consecutive experts of one token (four lanes per token, the
+    // workgroup's 64 tokens in one pass).  The selection bias of those experts is fetched
+    // now, behind the first stages, so that its latency hides behind the K loop: plain loads
+    // from clamped addresses (entries past T or E are loaded but never used) and nothing that
+    // reads the registers before the epilogue -- a select or a conditional copy here would
+    // make the wave wait for every load in flight, the stages included.  BIAS: 0 none, 1
+    // scalar loads, 2 16-byte loads (bias 16-byte aligned, E and the row stride multiples
+    // of 4: a group starting below E then lies inside the row).
+    constexpr int NV = EP / 4;
+    const int q = lane & 3;
+    const int tt = wave * 16 + (lane >> 2);
+    const int64_t t = tok0 + tt;
+    float bv[NV];
+    if constexpr (BIAS == 0) {
 #pragma unroll
-    for (int pass = 0; pass < 2; ++pass) {
-        const int64_t t = tok0 + pass * 32 + wave * 8 + (lane >> 3);
-        const int e0 = NV * q;
-        const float* bp = bias ? bias + t * bias_stride + e0 : nullptr;
-        if (bias && t < T && e0 + NV <= E && (reinterpret_cast<uintptr_t>(bp) & 15u) == 0) {
+        for (int j = 0; j < NV; ++j) bv[j] = 0.f;
+    } else {
+        const float* bp = bias + (t < T ? t : T - 1) * bias_stride;
+        if constexpr (BIAS == 2) {
 #pragma unroll
             for (int j = 0; j < NV; j += 4) {
-                const float4 v = *reinterpret_cast<const float4*>(bp + j);
-                bv[pass][j] = v.x;
-                bv[pass][j + 1] = v.y;
-                bv[pass][j + 2] = v.z;
-                bv[pass][j + 3] = v.w;
+                const float4 v = *reinterpret_cast<const float4*>(bp + min(NV * q + j, E - 4));
+                bv[j] = v.x;
+                bv[j + 1] = v.y;
+                bv[j + 2] = v.z;
+                bv[j + 3] = v.w;
             }
         } else {
 #pragma unroll
-            for (int j = 0; j < NV; ++j) bv[pass][j] = (bias && t < T && e0 + j < E) ? bp[j] : 0.f;
+            for (int j = 0; j < NV; ++j) bv[j] = bp[min(NV * q + j, E - 1)];
         }
     }
 
@@ -283,20 +440,25 @@ __global__ __launch_bounds__(kWaves * kWave) void route_lds_kernel(const bf16_t*
         wait_stages<LPW, NS>(issued - kc - 1);
         stage_barrier();
         if (issued < nk) issue();
+        // every fragment of the chunk is read before its MFMAs (one LDS latency per chunk)
         const unsigned char* st = smem + (kc % NS) * S::kChunkBytes;
+        bf16x8_t xf[kRK / 16], gf[kRK / 16][NBW];
 #pragma unroll
         for (int ks = 0; ks < kRK / 16; ++ks) {
             const int ch = 2 * ks + lhi;
             const int Rt = 32 * wt + l32;
-            const bf16x8_t xf = *reinterpret_cast<const bf16x8_t*>(st + Rt * 128 + ((ch ^ ((Rt >> 1) & 7)) << 4));
+            xf[ks] = *reinterpret_cast<const bf16x8_t*>(st + Rt * 128 + ((ch ^ ((Rt >> 1) & 7)) << 4));
 #pragma unroll
             for (int b = 0; b < NBW; ++b) {
                 const int Re = kRTok + we * (EP / 2) + 32 * b + l32;
-                const bf16x8_t gf =
-                    *reinterpret_cast<const bf16x8_t*>(st + Re * 128 + ((ch ^ ((Re >> 1) & 7)) << 4));
-                acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(gf, xf, acc[b], 0, 0, 0);
+                gf[ks][b] = *reinterpret_cast<const bf16x8_t*>(st + Re * 128 + ((ch ^ ((Re >> 1) & 7)) << 4));
             }
         }
+        __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the MFMAs
+#pragma unroll
+        for (int ks = 0; ks < kRK / 16; ++ks)
+#pragma unroll
+            for (int b = 0; b < NBW; ++b) acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(gf[ks][b], xf[ks], acc[b], 0, 0, 0);
     }
 
     // logits to LDS: D[expert][token] layout, lane = token 32 wt + l32, register i = expert
@@ -310,84 +472,58 @@ __global__ __launch_bounds__(kWaves * kWave) void route_lds_kernel(const bf16_t*
             part[(32 * wt + l32) * LDW + we * (EP / 2) + 32 * b + 8 * (i >> 2) + 4 * lhi + (i & 3)] = acc[b][i];
     __syncthreads();
 
-    // eight lanes per token, 32 tokens per pass; lane q holds experts NV q .. NV q + NV - 1
+    // four lanes per token; lane q holds experts NV q .. NV q + NV - 1 of token tt (read
+    // whole, padding included: the row has EP + 4 entries)
+    const float* lrow = part + tt * LDW + NV * q;
+    float lv[NV], sv[NV];
 #pragma unroll
-    for (int pass = 0; pass < 2; ++pass) {
-        const int tt = pass * 32 + wave * 8 + (lane >> 3);
-        const int64_t t = tok0 + tt;
-        float lv[NV], sv[NV];
-        float mx = -INFINITY;
-#pragma unroll
-        for (int j = 0; j < NV; ++j) {
-            const int e = NV * q + j;
-            const float v = part[tt * LDW + e];
-            const bool ok = e < E;
-            lv[j] = ok ? v : -INFINITY;
-            sv[j] = ok ? v + bv[pass][j] : -INFINITY;
-            mx = fmaxf(mx, lv[j]);
-        }
-#pragma unroll
-        for (int o = 1; o < 8; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
-        float den = 0.f;
-#pragma unroll
-        for (int j = 0; j < NV; ++j) den += (NV * q + j < E) ? expf(lv[j] - mx) : 0.f;
-#pragma unroll
-        for (int o = 1; o < 8; o <<= 1) den += __shfl_xor(den, o, kWave);
-
-        // k rounds of arg-max over the selection score; equal scores -> lower expert id
-        // (each lane scans its experts upward with a strict comparison, and the lane
-        // reduction prefers the lower id on ties)
-        uint32_t taken = 0;
-        float wsum = 0.f;
-        for (int j = 0; j < k; ++j) {
-            float bs = -INFINITY, bl = -INFINITY;
-            int be = 0x7fffffff;
-#pragma unroll
-            for (int jj = 0; jj < NV; ++jj) {
-                const int e = NV * q + jj;
-                if (e < E && !((taken >> jj) & 1u) && (sv[jj] > bs || be == 0x7fffffff)) {
-                    bs = sv[jj];
-                    bl = lv[jj];
-                    be = e;
-                }
-            }
-#pragma unroll
-            for (int o = 1; o < 8; o <<= 1) {
-                const float os = __shfl_xor(bs, o, kWave);
-                const float ol = __shfl_xor(bl, o, kWave);
-                const int oe = __shfl_xor(be, o, kWave);
-                if (oe != 0x7fffffff && (be == 0x7fffffff || os > bs || (os == bs && oe < be))) {
-                    bs = os;
-                    bl = ol;
-                    be = oe;
-                }
-            }
-            const bool found = be != 0x7fffffff;
-            if (found && be / NV == q) taken |= 1u << (be - NV * q);
-            const float p = found ? expf(bl - mx) / den : 0.f;
-            wsum += p;
-            if (q == 0 && t < T) {
-                idx[t * k + j] = found ? be : -1;
-                w[t * k + j] = p;
-            }
-        }
-        if (renorm && q == 0 && t < T)
-            for (int j = 0; j < k; ++j) w[t * k + j] = w[t * k + j] / wsum;
+    for (int j = 0; j < NV; j += 4) {
+        const float4 v = *reinterpret_cast<const float4*>(lrow + j);
+        lv[j] = v.x;
+        lv[j + 1] = v.y;
+        lv[j + 2] = v.z;
+        lv[j + 3] = v.w;
     }
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        sv[j] = NV * q + j < E ? lv[j] + bv[j] : -INFINITY;
+        lv[j] = NV * q + j < E ? lv[j] : -INFINITY;
+    }
+    const QuadPicks r = select_quad<NV>(lv, sv, q, E, k, renorm, t < T, t, idx, w);
+    if (k <= kQuadPicks && t < T) {
+        if (q < k) {
+            idx[t * k + q] = r.e0;
+            w[t * k + q] = renorm ? r.p0 / r.wsum : r.p0;
+        }
+        if (q + 4 < k) {
+            idx[t * k + q + 4] = r.e1;
+            w[t * k + q + 4] = renorm ? r.p1 / r.wsum : r.p1;
+        }
+    }
+}
+
+template <int NBW, int BIAS>
+hipError_t launch_route_lds_b(const void* x, int64_t T, int h, const void* wg, int E, int k, const float* bias,
+                              int64_t bias_stride, int renorm, int32_t* idx, float* w, hipStream_t s) {
+    constexpr size_t lds = RouteLds<NBW>::kBytes;
+    static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&route_lds_kernel<NBW, BIAS>),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                       static_cast<int>(lds));
+    if (attr != hipSuccess) return attr;
+    const dim3 grid(static_cast<unsigned>(ceil_div(T, kRTok)));
+    hipLaunchKernelGGL((route_lds_kernel<NBW, BIAS>), grid, dim3(kWaves * kWave), lds, s,
+                       static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(wg), T, h, E, k, bias, bias_stride,
+                       renorm, idx, w);
+    return hipGetLastError();
 }
 
 template <int NBW>
 hipError_t launch_route_lds(const void* x, int64_t T, int h, const void* wg, int E, int k, const float* bias,
                             int64_t bias_stride, int renorm, int32_t* idx, float* w, hipStream_t s) {
-    constexpr size_t lds = RouteLds<NBW>::kBytes;
-    static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&route_lds_kernel<NBW>),
-                                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                       static_cast<int>(lds));
-    if (attr != hipSuccess) return attr;
-    const dim3 grid(static_cast<unsigned>(ceil_div(T, kRTok)));
-    hipLaunchKernelGGL((route_lds_kernel<NBW>), grid, dim3(kWaves * kWave), lds, s, static_cast<const bf16_t*>(x),
-                       static_cast<const bf16_t*>(wg), T, h, E, k, bias, bias_stride, renorm, idx, w);
-    return hipGetLastError();
+    if (!bias) return launch_route_lds_b<NBW, 0>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, s);
+    if ((reinterpret_cast<uintptr_t>(bias) & 15u) == 0 && E % 4 == 0 && bias_stride % 4 == 0)
+        return launch_route_lds_b<NBW, 2>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, s);
+    return launch_route_lds_b<NBW, 1>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, s);
 }
 
 template <typename Tin, int NB>
