@@ -12,9 +12,10 @@
 //   gather  x_perm[p] = x[row_src[p]] with 16-byte vector copies
 // When the count table (experts x chunks) is small, the scan runs inside every rank
 // workgroup instead (dispatch_rank_scan: two launches).  Up to kFusedMaxA assignments,
-// count, scan and rank run as one kernel (same output): every chunk's workgroup counts all
-// assignments itself into per-wave LDS histograms, keeping the counts of the chunks before
-// its own apart, scans the totals, and ranks its chunk as above.
+// count, scan and rank run as one kernel (same output): every chunk's workgroup, 16 waves,
+// counts all assignments itself into per-wave LDS histograms, keeping the counts of the
+// chunks before its own apart, scans the totals, and ranks its chunk in one round (one
+// group of 64 per wave).
 // Integer atomics are used only for the LDS histograms, whose result does not depend on
 // their order.
 #include "common.h"
@@ -30,19 +31,32 @@ constexpr int kDispWaves = kDispThreads / kWave;
 constexpr int kPerWave = kDispatchChunk / kDispWaves;  // 256
 constexpr int kRounds = kPerWave / kWave;              // 4
 
+// The ids of this wave's kRounds groups of 64 assignments from a0 on (-1 past A): every load
+// is issued before any is used, from a clamped index, so that they make one memory round
+// trip (a load guarded by its own condition becomes a branch that waits for it).
+__device__ __forceinline__ void load_wave_ids(const int32_t* __restrict__ idx, int64_t A, int64_t a0, int lane,
+                                              int (&ev)[kRounds]) {
+#pragma unroll
+    for (int s = 0; s < kRounds; ++s) {
+        const int64_t a = a0 + s * kWave + lane;
+        ev[s] = idx[a < A ? a : A - 1];
+    }
+#pragma unroll
+    for (int s = 0; s < kRounds; ++s) ev[s] = a0 + s * kWave + lane < A ? ev[s] : -1;
+}
+
 __global__ __launch_bounds__(kDispThreads) void dispatch_count(const int32_t* __restrict__ idx, int64_t A,
                                                                int E, int nchunks, int32_t* __restrict__ cc) {
     __shared__ int hist[MOE_MAX_EXPERTS];
     for (int e = threadIdx.x; e < E; e += kDispThreads) hist[e] = 0;
     __syncthreads();
-    const int64_t base = static_cast<int64_t>(blockIdx.x) * kDispatchChunk;
-    for (int i = threadIdx.x; i < kDispatchChunk; i += kDispThreads) {
-        const int64_t a = base + i;
-        if (a < A) {
-            const int e = idx[a];
-            if (static_cast<unsigned>(e) < static_cast<unsigned>(E)) atomicAdd(&hist[e], 1);
-        }
-    }
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    int ev[kRounds];
+    load_wave_ids(idx, A, static_cast<int64_t>(blockIdx.x) * kDispatchChunk + wave * kPerWave, lane, ev);
+#pragma unroll
+    for (int s = 0; s < kRounds; ++s)
+        if (static_cast<unsigned>(ev[s]) < static_cast<unsigned>(E)) atomicAdd(&hist[ev[s]], 1);
     __syncthreads();
     for (int e = threadIdx.x; e < E; e += kDispThreads)
         cc[static_cast<int64_t>(e) * nchunks + blockIdx.x] = hist[e];
@@ -100,12 +114,10 @@ __global__ __launch_bounds__(kDispThreads) void dispatch_rank(const int32_t* __r
     __syncthreads();
     const int64_t a0 = static_cast<int64_t>(c) * kDispatchChunk + wave * kPerWave;
     int ev[kRounds];
+    load_wave_ids(idx, A, a0, lane, ev);
 #pragma unroll
-    for (int s = 0; s < kRounds; ++s) {
-        const int64_t a = a0 + s * kWave + lane;
-        ev[s] = (a < A) ? idx[a] : -1;
+    for (int s = 0; s < kRounds; ++s)
         if (static_cast<unsigned>(ev[s]) < static_cast<unsigned>(E)) atomicAdd(&wcnt[wave][ev[s]], 1);
-    }
     __syncthreads();
     for (int e = lane; e < E; e += kWave) {
         int b = base[static_cast<int64_t>(e) * nchunks + c];
@@ -163,33 +175,57 @@ __global__ __launch_bounds__(kDispThreads) void dispatch_rank_scan(const int32_t
     const int wave = threadIdx.x / kWave;
     const int c = blockIdx.x;
     const int64_t a0 = static_cast<int64_t>(c) * kDispatchChunk + wave * kPerWave;
-    // this chunk's ids and the whole count table, loaded together (one memory round trip)
+    // this chunk's ids and the whole count table, loaded together (one memory round trip):
+    // every load from a clamped index, issued before any is stored
     int ev[kRounds];
+    load_wave_ids(idx, A, a0, lane, ev);
+    constexpr int kTablePer = kRankScanMaxTable / kDispThreads;
+    const int L = E * nchunks;
+    int tv[kTablePer];
 #pragma unroll
-    for (int s = 0; s < kRounds; ++s) {
-        const int64_t a = a0 + s * kWave + lane;
-        ev[s] = (a < A) ? idx[a] : -1;
-    }
+    for (int u = 0; u < kTablePer; ++u)
+        if (u * kDispThreads < L) tv[u] = cc[min(static_cast<int>(threadIdx.x) + u * kDispThreads, L - 1)];
     // stored chunk-major with a padded row (E + 1 counters), so that both the copy and the
     // per-expert sums below touch distinct banks
-    const int L = E * nchunks;
-    for (int i = threadIdx.x; i < L; i += kDispThreads) {
+#pragma unroll
+    for (int u = 0; u < kTablePer; ++u) {
+        const int i = threadIdx.x + u * kDispThreads;
         const int e = i / nchunks, ch = i - e * nchunks;
-        table[ch * (E + 1) + e] = cc[i];
+        if (i < L) table[ch * (E + 1) + e] = tv[u];
     }
-    for (int e = lane; e < E; e += kWave) wcnt[wave][e] = 0;
     __syncthreads();
+    // each expert's total and its count in the chunks before this one: G = 256 / E threads
+    // per expert (G = 1 .. 256) sum every G-th chunk, then one thread per expert adds the G
+    // partial sums (integers: the order does not matter)
     static_assert(MOE_MAX_EXPERTS <= kDispThreads, "one expert per thread");
-    if (threadIdx.x < E) {
+    {
+        const int G = kDispThreads / E;
+        const int e = threadIdx.x % E, g = threadIdx.x / E;
         int t = 0, b = 0;
-        for (int i = 0; i < nchunks; ++i) {
-            const int v = table[i * (E + 1) + threadIdx.x];
-            t += v;
-            b += i < c ? v : 0;
+        if (g < G)
+            for (int i = g; i < nchunks; i += G) {
+                const int v = table[i * (E + 1) + e];
+                t += v;
+                b += i < c ? v : 0;
+            }
+        if (g < G) {
+            wcnt[0][threadIdx.x] = t;  // scratch for the partial sums (wcnt is cleared again below)
+            run[0][threadIdx.x] = b;
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < E) {
+        const int G = kDispThreads / E;
+        int t = 0, b = 0;
+        for (int g = 0; g < G; ++g) {
+            t += wcnt[0][g * E + threadIdx.x];
+            b += run[0][g * E + threadIdx.x];
         }
         tot[threadIdx.x] = t;
         before[threadIdx.x] = b;
     }
+    __syncthreads();
+    for (int e = lane; e < E; e += kWave) wcnt[wave][e] = 0;
     __syncthreads();
 #pragma unroll
     for (int s = 0; s < kRounds; ++s)
@@ -257,7 +293,6 @@ __global__ __launch_bounds__(kDispThreads) void dispatch_rank_scan(const int32_t
 }
 
 constexpr int64_t kFusedMaxA = 16384;
-constexpr int kFusedBatch = 16;  // groups of 64 assignments whose loads are issued together
 
 // Lanes of this wave whose expert equals this lane's (valid lanes only), from nbits ballots.
 __device__ __forceinline__ uint64_t same_expert_lanes(int e, bool valid, int nbits) {
@@ -270,52 +305,63 @@ __device__ __forceinline__ uint64_t same_expert_lanes(int e, bool valid, int nbi
     return peers;
 }
 
-__global__ __launch_bounds__(kDispThreads) void dispatch_fused(const int32_t* __restrict__ idx, int64_t A, int k,
-                                                               int E, int nbits, int32_t* __restrict__ counts,
-                                                               int32_t* __restrict__ offsets,
-                                                               int32_t* __restrict__ row_src,
-                                                               int32_t* __restrict__ pos_of) {
+// One workgroup of 16 waves per chunk of 1024 assignments (one group of 64 per wave), so
+// that counting every assignment is spread over 1024 threads and the chunk is ranked in a
+// single round.
+constexpr int kFusedThreads = 1024;
+constexpr int kFusedWaves = kFusedThreads / kWave;
+static_assert(kFusedWaves * kWave == kDispatchChunk, "one wave per 64 assignments of a chunk");
+constexpr int kFusedLoads = 8;  // groups of 64 assignments per wave whose loads go out together
+
+__global__ __launch_bounds__(kFusedThreads) void dispatch_fused(const int32_t* __restrict__ idx, int64_t A, int k,
+                                                                 int E, int nbits, int32_t* __restrict__ counts,
+                                                                 int32_t* __restrict__ offsets,
+                                                                 int32_t* __restrict__ row_src,
+                                                                 int32_t* __restrict__ pos_of) {
+    // per-wave histograms: all assignments (h_all) and those before this chunk (h_bef);
+    // h_all then holds each wave's counts within this chunk
+    __shared__ int h_all[kFusedWaves][MOE_MAX_EXPERTS];
+    __shared__ int h_bef[kFusedWaves][MOE_MAX_EXPERTS];
     __shared__ int tot[MOE_MAX_EXPERTS];
     __shared__ int before[MOE_MAX_EXPERTS];
     __shared__ int off[MOE_MAX_EXPERTS + 1];
-    __shared__ int wcnt[kDispWaves][MOE_MAX_EXPERTS];
-    __shared__ int run[kDispWaves][MOE_MAX_EXPERTS];
-    __shared__ int wtot[kDispWaves][MOE_MAX_EXPERTS];
-    __shared__ int wbef[kDispWaves][MOE_MAX_EXPERTS];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const int c = blockIdx.x;
     const int64_t cbeg = static_cast<int64_t>(c) * kDispatchChunk;
-    for (int e = lane; e < E; e += kWave) wcnt[wave][e] = wtot[wave][e] = wbef[wave][e] = 0;
+    // this lane's assignment of the chunk, loaded first (its latency hides behind the count)
+    const int64_t my_a = cbeg + wave * kWave + lane;
+    int my_e = idx[my_a < A ? my_a : A - 1];
+    for (int e = lane; e < E; e += kWave) h_all[wave][e] = h_bef[wave][e] = 0;
     __syncthreads();
-    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 
-    // every assignment, 64 at a time per wave (kFusedBatch groups' loads in flight together),
-    // into this wave's histograms
-    for (int64_t b0 = static_cast<int64_t>(wave) * kWave; b0 < A; b0 += kDispThreads * kFusedBatch) {
-        int eb[kFusedBatch];
+    // every assignment into this wave's histograms, kFusedLoads groups of 64 per round with
+    // their loads issued together (clamped indices; a group lies wholly before the chunk or
+    // wholly in or after it, as chunks are multiples of 64)
+    for (int64_t b0 = static_cast<int64_t>(wave) * kWave; b0 < A; b0 += kFusedThreads * kFusedLoads) {
+        int eb[kFusedLoads];
 #pragma unroll
-        for (int u = 0; u < kFusedBatch; ++u) {
-            const int64_t a = b0 + static_cast<int64_t>(u) * kDispThreads + lane;
-            eb[u] = (a < A) ? idx[a] : -1;
+        for (int u = 0; u < kFusedLoads; ++u) {
+            const int64_t a = b0 + static_cast<int64_t>(u) * kFusedThreads + lane;
+            eb[u] = idx[a < A ? a : A - 1];
         }
 #pragma unroll
-        for (int u = 0; u < kFusedBatch; ++u) {
-            const int64_t a = b0 + static_cast<int64_t>(u) * kDispThreads + lane;
-            const int e = eb[u];
+        for (int u = 0; u < kFusedLoads; ++u) {
+            const int64_t g0 = b0 + static_cast<int64_t>(u) * kFusedThreads;
+            const int e = g0 + lane < A ? eb[u] : -1;
             if (static_cast<unsigned>(e) < static_cast<unsigned>(E)) {
-                atomicAdd(&wtot[wave][e], 1);
-                if (a < cbeg) atomicAdd(&wbef[wave][e], 1);
+                atomicAdd(&h_all[wave][e], 1);
+                if (g0 < cbeg) atomicAdd(&h_bef[wave][e], 1);
             }
         }
     }
     __syncthreads();
-    for (int e = threadIdx.x; e < E; e += kDispThreads) {
+    for (int e = threadIdx.x; e < E; e += kFusedThreads) {
         int t = 0, b = 0;
 #pragma unroll
-        for (int w = 0; w < kDispWaves; ++w) {
-            t += wtot[w][e];
-            b += wbef[w][e];
+        for (int w = 0; w < kFusedWaves; ++w) {
+            t += h_all[w][e];
+            b += h_bef[w][e];
         }
         tot[e] = t;
         before[e] = b;
@@ -344,47 +390,31 @@ __global__ __launch_bounds__(kDispThreads) void dispatch_fused(const int32_t* __
         }
         if (lane == kWave - 1) off[E] = incl;
     }
+    // each wave's counts within the chunk (h_all is free again after the sums above)
+    my_e = my_a < A ? my_e : -1;
+    const bool valid = static_cast<unsigned>(my_e) < static_cast<unsigned>(E);
+    const uint64_t peers = same_expert_lanes(my_e, valid, nbits);
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const int rank = __popcll(peers & lt);
+    for (int e = lane; e < E; e += kWave) h_all[wave][e] = 0;
     __syncthreads();
+    if (valid && rank == 0) h_all[wave][my_e] = __popcll(peers);
     if (c == 0) {
-        for (int e = threadIdx.x; e <= E; e += kDispThreads) {
+        for (int e = threadIdx.x; e <= E; e += kFusedThreads) {
             offsets[e] = off[e];
             if (e < E) counts[e] = tot[e];
         }
     }
+    __syncthreads();
 
-    // rank this chunk's assignments (as in dispatch_rank, with base = off + before)
-    const int64_t a0 = cbeg + wave * kPerWave;
-    int ev[kRounds];
-#pragma unroll
-    for (int s = 0; s < kRounds; ++s) {
-        const int64_t a = a0 + s * kWave + lane;
-        ev[s] = (a < A) ? idx[a] : -1;
-        if (static_cast<unsigned>(ev[s]) < static_cast<unsigned>(E)) atomicAdd(&wcnt[wave][ev[s]], 1);
-    }
-    __syncthreads();
-    for (int e = lane; e < E; e += kWave) {
-        int b = off[e] + before[e];
-        for (int w = 0; w < wave; ++w) b += wcnt[w][e];
-        run[wave][e] = b;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int s = 0; s < kRounds; ++s) {
-        const int64_t a = a0 + s * kWave + lane;
-        const int e = ev[s];
-        const bool valid = static_cast<unsigned>(e) < static_cast<unsigned>(E);
-        const uint64_t peers = same_expert_lanes(e, valid, nbits);
-        const int rank = __popcll(peers & lt);
-        if (valid) {
-            const int pos = run[wave][e] + rank;
-            pos_of[a] = pos;
-            if (pos >= 0 && pos < A) row_src[pos] = static_cast<int32_t>(a / k);
-        } else if (a < A) {
-            pos_of[a] = -1;
-        }
-        __syncthreads();  // every lane has read run[] before the group leaders advance it
-        if (valid && rank == 0) run[wave][e] += __popcll(peers);
-        __syncthreads();
+    // position = expert start + earlier chunks + earlier waves of this chunk + earlier lanes
+    if (valid) {
+        int pos = off[my_e] + before[my_e] + rank;
+        for (int w = 0; w < wave; ++w) pos += h_all[w][my_e];
+        pos_of[my_a] = pos;
+        if (pos >= 0 && pos < A) row_src[pos] = static_cast<int32_t>(my_a / k);
+    } else if (my_a < A) {
+        pos_of[my_a] = -1;
     }
 }
 
@@ -431,7 +461,7 @@ hipError_t launch_dispatch(const int32_t* idx, int64_t T, int k, int E, const vo
     int nbits = 0;
     while ((1 << nbits) < E) ++nbits;
     if (nchunks > 0 && A <= kFusedMaxA) {
-        hipLaunchKernelGGL(dispatch_fused, dim3(nchunks), dim3(kDispThreads), 0, s, idx, A, k, E, nbits, counts,
+        hipLaunchKernelGGL(dispatch_fused, dim3(nchunks), dim3(kFusedThreads), 0, s, idx, A, k, E, nbits, counts,
                            offsets, row_src, pos_of);
     } else {
         if (nchunks > 0) {
