@@ -176,6 +176,27 @@ moe_status moe_expert_ffn_shard_gather(const void *x, int64_t T, const int32_t *
                                        const void *packed, void *y_perm, moe_dtype ydt, void *ws,
                                        size_t ws_bytes, hipStream_t stream);
 
+/* Steps 4 and 5 together for any k (Algorithm 1's expert computation and weighted
+ * combination): moe_expert_ffn_shard_gather on rows_max = T * k followed by moe_combine,
+ * with the same y bit for bit.  When the second product's K is split (calls of at most 512
+ * bf16 or 1024 fp32 rows, the decode-sized ones), the parts' sum and the combine run as one
+ * launch: each token's rows are summed over the parts, rounded to ydt exactly as y_perm
+ * would hold them, weighted and accumulated in pick order, and y_perm is not written;
+ * otherwise y_perm is written as by moe_expert_ffn_shard_gather and then combined.
+ *   x, row_src, offsets, E, h, f, act, dt, packed, ydt, ws: as moe_expert_ffn_shard_gather
+ *            with A_max = T * k (T * k < 2^31)
+ *   pos_of   [T, k] int32 from moe_dispatch;  topk_w [T, k] fp32 from moe_route
+ *   y_perm   [T * k, h] dtype ydt scratch (written only when K is not split)
+ *   y        [T, h] out, dtype out_dt
+ *   y_perm_written  optional host int: set to 1 if y_perm was written, else 0 (may be NULL) */
+moe_status moe_expert_ffn_shard_gather_combine(const void *x, int64_t T, const int32_t *row_src,
+                                               const int32_t *offsets, const int32_t *pos_of,
+                                               const float *topk_w, int32_t k, int32_t E, int64_t h,
+                                               int64_t f, moe_act act, moe_dtype dt, const void *packed,
+                                               void *y_perm, moe_dtype ydt, void *y, moe_dtype out_dt,
+                                               int32_t *y_perm_written, void *ws, size_t ws_bytes,
+                                               hipStream_t stream);
+
 /* Steps 4 and 5 together for top-1 routing (k = 1): the expert step reads its rows through
  * row_src and its down-projection epilogue writes each token's gate-weighted result
  * straight into y, so neither x_perm nor y_perm nor moe_combine is needed:

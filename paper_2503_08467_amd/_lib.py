@@ -34,6 +34,8 @@ SIGNATURES = {
     "moe_expert_ffn_shard": (_ST, [_P, _P, _I64, _I32, _I64, _I64, _ST, _ST, _P, _P, _ST, _P, _SZ, _P]),
     "moe_expert_ffn_shard_gather": (_ST, [_P, _I64, _P, _P, _I64, _I32, _I64, _I64, _ST, _ST, _P, _P, _ST, _P, _SZ,
                                           _P]),
+    "moe_expert_ffn_shard_gather_combine": (_ST, [_P, _I64, _P, _P, _P, _P, _I32, _I32, _I64, _I64, _ST, _ST, _P, _P,
+                                                  _ST, _P, _ST, _P, _P, _SZ, _P]),
     "moe_expert_ffn_shard_top1": (_ST, [_P, _I64, _P, _P, _P, _I32, _I64, _I64, _ST, _ST, _P, _P, _ST, _P, _SZ, _P]),
     "moe_expert_ffn_shard_per_expert": (_ST, [_P, _P, _P, _I64, _I32, _I64, _I64, _ST, _ST, _P, _P, _ST, _P, _SZ,
                                               _P]),

@@ -194,6 +194,38 @@ moe_status moe_expert_ffn_shard_gather(const void* x, int64_t T, const int32_t* 
                                            w2t, y_perm, ydt == MOE_BF16, ws, stream));
 }
 
+moe_status moe_expert_ffn_shard_gather_combine(const void* x, int64_t T, const int32_t* row_src,
+                                               const int32_t* offsets, const int32_t* pos_of, const float* topk_w,
+                                               int32_t k, int32_t E, int64_t h, int64_t f, moe_act act, moe_dtype dt,
+                                               const void* packed, void* y_perm, moe_dtype ydt, void* y,
+                                               moe_dtype out_dt, int32_t* y_perm_written, void* ws, size_t ws_bytes,
+                                               hipStream_t stream) {
+    if (k < 1 || T < 0 || T * static_cast<int64_t>(k) >= INT32_MAX || !valid_dtype(out_dt)) return MOE_ERR_INVALID_ARG;
+    const int64_t A_max = T * k;
+    const moe_status st = ffn_check(x, offsets, A_max, E, h, f, act, dt, packed, y_perm, ydt, ws, ws_bytes);
+    if (st != MOE_OK) return st;
+    const bool any = T > 0;
+    if (!ok_ptr(row_src, any) || !ok_ptr(pos_of, any) || !ok_ptr(y, any) ||
+        (any && (!topk_w || (reinterpret_cast<uintptr_t>(topk_w) & 3u))))
+        return MOE_ERR_INVALID_ARG;
+    if (T * h * elem_bytes(dt) >= (int64_t(1) << 32)) return MOE_ERR_UNSUPPORTED;
+    const size_t mb = packed_matrix_bytes(E, h, f, dt);
+    const unsigned char* base = static_cast<const unsigned char*>(packed);
+    const bool swiglu = act == MOE_ACT_SWIGLU;
+    const void* w1t = base;
+    const void* w3t = swiglu ? base + mb : nullptr;
+    const void* w2t = base + (swiglu ? 2 : 1) * mb;
+    bool written = true;
+    moe_status out = MOE_OK;
+    if (any)
+        out = from_hip(moe::launch_ffn_gather_combine(x, T, row_src, offsets, k, E, static_cast<int>(h),
+                                                      moe_padded_inner_width(f), static_cast<int>(act), dt == MOE_BF16,
+                                                      w1t, w3t, w2t, y_perm, ydt == MOE_BF16, pos_of, topk_w, y,
+                                                      out_dt == MOE_BF16, ws, stream, &written));
+    if (y_perm_written) *y_perm_written = written ? 1 : 0;
+    return out;
+}
+
 moe_status moe_expert_ffn_shard_top1(const void* x, int64_t T, const int32_t* row_src, const float* topk_w,
                                      const int32_t* offsets, int32_t E, int64_t h, int64_t f, moe_act act, moe_dtype dt,
                                      const void* packed, void* y, moe_dtype out_dt, void* ws, size_t ws_bytes,

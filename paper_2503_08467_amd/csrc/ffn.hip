@@ -1417,10 +1417,11 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_f32_lds(GroupedGemm g) {
 // out[p] = sum over s of partial[s][p] (s ascending) for the grouped rows p of the call,
 // [offsets[0], offsets[E]); with scatter (top-1), out[t] = w[t] * that sum for
 // t = scatter[p] instead (the down-projection's own epilogue, applied after the parts
-// meet).  N % 4 == 0.
+// meet).  N % 4 == 0.  S (2, 4 or 8 parts) is a template argument so that a thread's S
+// loads are issued together (one memory round trip) before the sum.
 
-template <bool OB>
-__global__ __launch_bounds__(256) void split_reduce(const float* __restrict__ partial, int S, int64_t rows_max,
+template <bool OB, int S>
+__global__ __launch_bounds__(256) void split_reduce(const float* __restrict__ partial, int64_t rows_max,
                                                      int N, const int32_t* __restrict__ offsets, int E,
                                                      void* __restrict__ out, int ldo,
                                                      const int32_t* __restrict__ scatter,
@@ -1433,13 +1434,17 @@ __global__ __launch_bounds__(256) void split_reduce(const float* __restrict__ pa
          i += static_cast<int64_t>(gridDim.x) * 256) {
         const int64_t p = p0 + i / nv;
         const int c = static_cast<int>(i % nv) * 4;
-        float4 v = *reinterpret_cast<const float4*>(partial + p * N + c);
+        float4 u[S];
+#pragma unroll
+        for (int s = 0; s < S; ++s)
+            u[s] = *reinterpret_cast<const float4*>(partial + (static_cast<int64_t>(s) * rows_max + p) * N + c);
+        float4 v = u[0];
+#pragma unroll
         for (int s = 1; s < S; ++s) {
-            const float4 u = *reinterpret_cast<const float4*>(partial + (static_cast<int64_t>(s) * rows_max + p) * N + c);
-            v.x += u.x;
-            v.y += u.y;
-            v.z += u.z;
-            v.w += u.w;
+            v.x += u[s].x;
+            v.y += u[s].y;
+            v.z += u[s].z;
+            v.w += u[s].w;
         }
         int64_t row = p;
         if (scatter) {
@@ -1459,6 +1464,74 @@ __global__ __launch_bounds__(256) void split_reduce(const float* __restrict__ pa
         } else {
             *reinterpret_cast<float4*>(static_cast<float*>(out) + row * ldo + c) = v;
         }
+    }
+}
+
+
+// Steps 4 and 5 together when the second product's K is split: for token t and 8 columns,
+//     y[t] = sum over picks j of w[t, j] * round_ydt(sum over s of partial[s][pos_of[t, j]])
+// -- exactly split_reduce's sum (parts in order), rounded to y_perm's type as split_reduce
+// stores it, then combine's weighted sum (fp32, pick order, invalid picks skipped) rounded
+// once: the same bits as the two launches, without writing or reading y_perm.
+template <bool YB, bool OB, int S>
+__global__ __launch_bounds__(256) void split_combine(const float* __restrict__ partial, int64_t rows_max,
+                                                     int h, const int32_t* __restrict__ pos_of,
+                                                     const float* __restrict__ w, int64_t T, int k,
+                                                     void* __restrict__ y) {
+    const int nv = h / 8;
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= T * nv) return;
+    const int64_t t = i / nv;
+    const int c = static_cast<int>(i - t * nv) * 8;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < k; ++j) {
+        const int32_t p = pos_of[t * k + j];
+        if (p < 0 || p >= T * k) continue;
+        const float wt = w[t * k + j];
+        const float* src = partial + static_cast<int64_t>(p) * h + c;
+        float4 u[S], v[S];
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            const float* q = src + static_cast<int64_t>(s) * rows_max * h;
+            u[s] = *reinterpret_cast<const float4*>(q);
+            v[s] = *reinterpret_cast<const float4*>(q + 4);
+        }
+        float4 a = u[0], b = v[0];
+#pragma unroll
+        for (int s = 1; s < S; ++s) {
+            a.x += u[s].x;
+            a.y += u[s].y;
+            a.z += u[s].z;
+            a.w += u[s].w;
+            b.x += v[s].x;
+            b.y += v[s].y;
+            b.z += v[s].z;
+            b.w += v[s].w;
+        }
+        float r[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+        if (YB) {
+            // y_perm's bf16 rounding, as split_reduce stores it and combine reads it back
+#pragma unroll
+            for (int q = 0; q < 8; q += 2) {
+                const uint32_t pk = pack_bf16x2(r[q], r[q + 1]);
+                r[q] = __uint_as_float(pk << 16);
+                r[q + 1] = __uint_as_float(pk & 0xffff0000u);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[q] += wt * r[q];
+    }
+    if (OB) {
+        uint4 q;
+        q.x = pack_bf16x2(acc[0], acc[1]);
+        q.y = pack_bf16x2(acc[2], acc[3]);
+        q.z = pack_bf16x2(acc[4], acc[5]);
+        q.w = pack_bf16x2(acc[6], acc[7]);
+        *reinterpret_cast<uint4*>(static_cast<bf16_t*>(y) + t * h + c) = q;
+    } else {
+        float4* o = reinterpret_cast<float4*>(static_cast<float*>(y) + t * h + c);
+        o[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+        o[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
     }
 }
 
@@ -1608,10 +1681,76 @@ hipError_t gemm1(bool bf16, GroupedGemm g, int64_t A_max, hipStream_t s) {
 
 // Both matmuls of the expert step.  grid_rows sizes the launches (an upper bound of the
 // rows the offsets describe); rows_max is the row count of x_perm, H and y_perm.
+// Step 5 folded into the expert step (CombineArgs given and the second product split): the
+// parts' sum goes straight into y through split_combine instead of into y_perm.
+struct CombineArgs {
+    const int32_t* pos_of;
+    const float* w;
+    int64_t T;
+    int k;
+    void* y;
+    bool y_bf16;
+};
+
+
+template <bool OB, int S>
+hipError_t launch_split_reduce_t(const float* partial, int64_t rows_max, int h, int64_t grid_rows,
+                                 const int32_t* offsets, int E, void* out, const int32_t* scatter,
+                                 const float* scatter_w, int64_t c_rows, hipStream_t s) {
+    const int64_t n4 = grid_rows * (h / 4);
+    const int blocks = static_cast<int>(std::min<int64_t>(ceil_div(n4, 256), 8LL * device_cus()));
+    hipLaunchKernelGGL((split_reduce<OB, S>), dim3(blocks), dim3(256), 0, s, partial, rows_max, h, offsets, E, out, h,
+                       scatter, scatter_w, c_rows);
+    return hipGetLastError();
+}
+
+// S = the down-projection's K parts: 2, 4 or 8 (down_ksplit)
+hipError_t launch_split_reduce(bool ob, int S, const float* partial, int64_t rows_max, int h, int64_t grid_rows,
+                               const int32_t* offsets, int E, void* out, const int32_t* scatter,
+                               const float* scatter_w, int64_t c_rows, hipStream_t s) {
+#define MOE_SPLIT_REDUCE(OBV, SV) \
+    return launch_split_reduce_t<OBV, SV>(partial, rows_max, h, grid_rows, offsets, E, out, scatter, scatter_w, c_rows, s)
+    if (ob) {
+        if (S == 2) MOE_SPLIT_REDUCE(true, 2);
+        if (S == 4) MOE_SPLIT_REDUCE(true, 4);
+        if (S == 8) MOE_SPLIT_REDUCE(true, 8);
+    } else {
+        if (S == 2) MOE_SPLIT_REDUCE(false, 2);
+        if (S == 4) MOE_SPLIT_REDUCE(false, 4);
+        if (S == 8) MOE_SPLIT_REDUCE(false, 8);
+    }
+#undef MOE_SPLIT_REDUCE
+    return hipErrorInvalidValue;
+}
+
+template <bool YB, bool OB, int S>
+hipError_t launch_split_combine_t(const float* partial, int64_t rows_max, int h, const CombineArgs& c, hipStream_t s) {
+    const dim3 grid(static_cast<unsigned>(ceil_div(c.T * (h / 8), 256)));
+    hipLaunchKernelGGL((split_combine<YB, OB, S>), grid, dim3(256), 0, s, partial, rows_max, h, c.pos_of, c.w, c.T,
+                       c.k, c.y);
+    return hipGetLastError();
+}
+
+hipError_t launch_split_combine(bool yb, int S, const float* partial, int64_t rows_max, int h, const CombineArgs& c,
+                                hipStream_t s) {
+#define MOE_SPLIT_COMBINE(YBV, OBV)                                                              \
+    do {                                                                                       \
+        if (S == 2) return launch_split_combine_t<YBV, OBV, 2>(partial, rows_max, h, c, s);   \
+        if (S == 4) return launch_split_combine_t<YBV, OBV, 4>(partial, rows_max, h, c, s);   \
+        if (S == 8) return launch_split_combine_t<YBV, OBV, 8>(partial, rows_max, h, c, s);   \
+    } while (0)
+    if (yb && c.y_bf16) MOE_SPLIT_COMBINE(true, true);
+    else if (yb) MOE_SPLIT_COMBINE(true, false);
+    else if (c.y_bf16) MOE_SPLIT_COMBINE(false, true);
+    else MOE_SPLIT_COMBINE(false, false);
+#undef MOE_SPLIT_COMBINE
+    return hipErrorInvalidValue;
+}
+
 hipError_t ffn_pair(const void* x_perm, const int32_t* offsets, int64_t grid_rows, int64_t rows_max, int E,
                     int h, int64_t fp, int act, bool bf16, const void* w1t, const void* w3t, const void* w2t,
                     void* y_perm, bool y_bf16, void* hbuf, hipStream_t s, const int32_t* gather = nullptr,
-                    int64_t a_rows = 0, const float* scatter_w = nullptr) {
+                    int64_t a_rows = 0, const float* scatter_w = nullptr, const CombineArgs* comb = nullptr) {
     if (grid_rows == 0) return hipSuccess;
     GroupedGemm g1{};
     g1.a = x_perm;
@@ -1665,15 +1804,12 @@ hipError_t ffn_pair(const void* x_perm, const int32_t* offsets, int64_t grid_row
     else
         err = run_f32<kEpiNone, false>(g2, grid_rows, s);  // partial tiles only
     if (err != hipSuccess) return err;
-    const int64_t n4 = grid_rows * (h / 4);
-    const int blocks = static_cast<int>(std::min<int64_t>(ceil_div(n4, 256), 8LL * device_cus()));
-    if (y_bf16)
-        hipLaunchKernelGGL(split_reduce<true>, dim3(blocks), dim3(256), 0, s, g2.partial, g2.ksplit, rows_max, h,
-                           offsets, E, y_perm, h, g2.scatter, g2.scatter_w, g2.c_rows);
-    else
-        hipLaunchKernelGGL(split_reduce<false>, dim3(blocks), dim3(256), 0, s, g2.partial, g2.ksplit, rows_max, h,
-                           offsets, E, y_perm, h, g2.scatter, g2.scatter_w, g2.c_rows);
-    return hipGetLastError();
+    if (comb) {
+        if (comb->T == 0) return hipSuccess;
+        return launch_split_combine(y_bf16, g2.ksplit, g2.partial, rows_max, h, *comb, s);
+    }
+    return launch_split_reduce(y_bf16, g2.ksplit, g2.partial, rows_max, h, grid_rows, offsets, E, y_perm,
+                               g2.scatter, g2.scatter_w, g2.c_rows, s);
 }
 
 }  // namespace
@@ -1688,6 +1824,25 @@ hipError_t launch_ffn_gather(const void* x, int64_t T, const int32_t* row_src, c
                              int E, int h, int64_t fp, int act, bool bf16, const void* w1t, const void* w3t,
                              const void* w2t, void* y_perm, bool y_bf16, void* hbuf, hipStream_t s) {
     return ffn_pair(x, offsets, A_max, A_max, E, h, fp, act, bf16, w1t, w3t, w2t, y_perm, y_bf16, hbuf, s, row_src, T);
+}
+
+hipError_t launch_ffn_gather_combine(const void* x, int64_t T, const int32_t* row_src, const int32_t* offsets, int k,
+                                     int E, int h, int64_t fp, int act, bool bf16, const void* w1t, const void* w3t,
+                                     const void* w2t, void* y_perm, bool y_bf16, const int32_t* pos_of,
+                                     const float* topk_w, void* y, bool out_bf16, void* hbuf, hipStream_t s,
+                                     bool* y_perm_written) {
+    const int64_t A_max = T * k;
+    const bool split = down_ksplit(A_max, fp, bf16) > 1;
+    *y_perm_written = !split;
+    if (split) {
+        const CombineArgs comb{pos_of, topk_w, T, k, y, out_bf16};
+        return ffn_pair(x, offsets, A_max, A_max, E, h, fp, act, bf16, w1t, w3t, w2t, y_perm, y_bf16, hbuf, s,
+                        row_src, T, nullptr, &comb);
+    }
+    const hipError_t err =
+        ffn_pair(x, offsets, A_max, A_max, E, h, fp, act, bf16, w1t, w3t, w2t, y_perm, y_bf16, hbuf, s, row_src, T);
+    if (err != hipSuccess) return err;
+    return launch_combine(y_perm, y_bf16, pos_of, topk_w, T, k, h, y, out_bf16, s);
 }
 
 // One expert at a time: expert e's segment is the one-expert grouping (offsets + e), its

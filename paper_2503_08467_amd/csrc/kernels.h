@@ -61,6 +61,14 @@ hipError_t launch_ffn_gather(const void* x, int64_t T, const int32_t* row_src, c
                              int E, int h, int64_t fp, int act, bool bf16, const void* w1t, const void* w3t,
                              const void* w2t, void* y_perm, bool y_bf16, void* hbuf, hipStream_t s);
 
+// launch_ffn_gather followed by launch_combine; when the second product's K is split, its
+// parts' sum and the combine run as one kernel and y_perm is not written (*y_perm_written).
+hipError_t launch_ffn_gather_combine(const void* x, int64_t T, const int32_t* row_src, const int32_t* offsets, int k,
+                                     int E, int h, int64_t fp, int act, bool bf16, const void* w1t, const void* w3t,
+                                     const void* w2t, void* y_perm, bool y_bf16, const int32_t* pos_of,
+                                     const float* topk_w, void* y, bool out_bf16, void* hbuf, hipStream_t s,
+                                     bool* y_perm_written);
+
 hipError_t launch_ffn_top1(const void* x, int64_t T, const int32_t* row_src, const float* topk_w,
                            const int32_t* offsets, int64_t A_max, int E, int h, int64_t fp, int act, bool bf16,
                            const void* w1t, const void* w3t, const void* w2t, void* y, bool y_bf16, void* hbuf,

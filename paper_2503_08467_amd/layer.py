@@ -6,6 +6,7 @@ memory and the stream (the current stream of the tensors' device unless one is g
 """
 from __future__ import annotations
 
+import ctypes
 import dataclasses
 from typing import Optional
 
@@ -219,6 +220,40 @@ def expert_ffn_shard_gather(x: torch.Tensor, row_src: torch.Tensor, offsets: tor
     return out
 
 
+def expert_ffn_shard_gather_combine(x: torch.Tensor, row_src: torch.Tensor, offsets: torch.Tensor,
+                                    pos_of: torch.Tensor, topk_w: torch.Tensor, packed: PackedShard,
+                                    y_perm: Optional[torch.Tensor] = None, out_dtype: Optional[torch.dtype] = None,
+                                    out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                                    stream=None):
+    """Steps 4 and 5 for any k: the gathered expert step and the weighted combine in one call
+    (one launch for both when the second product's K is split).  Returns (y, y_perm or None
+    when y_perm was not written)."""
+    _dev(x, "x"), _dev(row_src, "row_src"), _dev(offsets, "offsets"), _dev(pos_of, "pos_of"), _dev(topk_w, "topk_w")
+    if x.dtype != packed.dtype:
+        raise TypeError("x must have the packed weights' dtype")
+    if row_src.dtype != torch.int32 or pos_of.dtype != torch.int32 or topk_w.dtype != torch.float32:
+        raise TypeError("row_src and pos_of must be int32, topk_w float32")
+    T = x.shape[0]
+    if pos_of.dim() != 2 or pos_of.shape[0] != T or topk_w.shape != pos_of.shape:
+        raise ValueError("pos_of and topk_w must be [T, k]")
+    k = pos_of.shape[1]
+    if row_src.numel() < T * k:
+        raise ValueError("row_src needs T * k entries")
+    out_dtype = out_dtype or x.dtype
+    if y_perm is None:
+        y_perm = torch.empty((T * k, packed.h), dtype=x.dtype, device=x.device)
+    if out is None:
+        out = torch.empty((T, packed.h), dtype=out_dtype, device=x.device)
+    if ws is None:
+        ws = torch.empty(max(ffn_workspace_size(T * k, packed), 16), dtype=torch.uint8, device=x.device)
+    written = ctypes.c_int32(0)
+    _lib.call("moe_expert_ffn_shard_gather_combine", _ptr(x), T, _ptr(row_src), _ptr(offsets), _ptr(pos_of),
+              _ptr(topk_w), k, packed.E, packed.h, packed.f, _lib.ACTS[packed.act], _DT[packed.dtype],
+              _ptr(packed.buf), _ptr(y_perm), _dt(y_perm), _ptr(out), _dt(out), ctypes.addressof(written),
+              _ptr(ws), ws.numel(), _stream(x, stream))
+    return out, (y_perm if written.value else None)
+
+
 def expert_ffn_shard_top1(x: torch.Tensor, row_src: torch.Tensor, topk_w: torch.Tensor, offsets: torch.Tensor,
                           packed: PackedShard, out_dtype: Optional[torch.dtype] = None,
                           out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
@@ -337,12 +372,14 @@ class MoEShardLayer:
             y = expert_ffn_shard_top1(x, d.row_src, w.view(-1), d.offsets, self.packed, out=self.y[:T], ws=self.fws)
         else:
             if d.x_perm is None:
-                y_perm = expert_ffn_shard_gather(x, d.row_src, d.offsets, self.packed, A_max=T * k,
-                                                 out=self.y_perm[:T * k], ws=self.fws)
+                # Steps 4 and 5 in one call (one launch for the split sum and the combine when
+                # the second product's K is split; y_perm is then not written)
+                y, y_perm = expert_ffn_shard_gather_combine(x, d.row_src, d.offsets, d.pos_of, w, self.packed,
+                                                            y_perm=self.y_perm[:T * k], out=self.y[:T], ws=self.fws)
             else:
                 y_perm = expert_ffn_shard(d.x_perm, d.offsets, self.packed, A_max=T * k, out=self.y_perm[:T * k],
                                           ws=self.fws)
-            y = combine(y_perm, d.pos_of, w, out=self.y[:T])
+                y = combine(y_perm, d.pos_of, w, out=self.y[:T])
         self.last = dict(idx=idx, w=w, dispatch=d, y_perm=y_perm)
         return y
 

@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 14, names
+    assert len(names) == 15, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(_lib.SIGNATURES)
@@ -244,3 +244,26 @@ def test_noalloc_rejects_calls_beyond_its_static_array(lib):
     st = lib.moe_expert_ffn_shard_noalloc(A16 + 4, A16, big, E, h, f, _lib.MOE_ACT_GELU, _lib.MOE_BF16, A16, A16,
                                           _lib.MOE_BF16, None)
     assert st == _lib.MOE_ERR_INVALID_ARG
+
+
+def test_gather_combine_rejects_bad_arguments(lib):
+    """The one-call expert step plus combine checks k, the output dtype and its pointers
+    before any launch."""
+    T, k, E, h, f = 64, 2, 4, 64, 32
+    ws = lib.moe_ffn_workspace_size(T * k, E, h, f, _lib.MOE_ACT_GELU, _lib.MOE_BF16)
+    flag = ctypes.c_int32(7)
+
+    def call(k=k, pos=A16, w=A16, y=A16, out_dt=_lib.MOE_BF16, T=T):
+        return lib.moe_expert_ffn_shard_gather_combine(A16, T, A16, A16, pos, w, k, E, h, f, _lib.MOE_ACT_GELU,
+                                                       _lib.MOE_BF16, A16, A16, _lib.MOE_BF16, y, out_dt,
+                                                       ctypes.addressof(flag), A16, ws, None)
+    assert call(k=0) == _lib.MOE_ERR_INVALID_ARG
+    assert call(pos=None) == _lib.MOE_ERR_INVALID_ARG
+    assert call(w=None) == _lib.MOE_ERR_INVALID_ARG
+    assert call(w=A16 + 2) == _lib.MOE_ERR_INVALID_ARG
+    assert call(y=None) == _lib.MOE_ERR_INVALID_ARG
+    assert call(out_dt=9) == _lib.MOE_ERR_INVALID_ARG
+    assert flag.value == 7  # untouched by a rejected call
+    # no tokens: nothing to launch, nothing written
+    assert call(T=0, pos=None, w=None, y=None) == _lib.MOE_OK
+    assert flag.value == 1

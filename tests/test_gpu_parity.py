@@ -341,6 +341,53 @@ def test_gathered_rows_match_x_perm(dtype, act, T, k, E, h, f):
     assert rowwise(np_of(y_gath[:n]), ref) <= TOL[dtype]
 
 
+@pytest.mark.parametrize("dtype,out_dtype", [("bf16", "bf16"), ("bf16", "f32"), ("f32", "f32"), ("f32", "bf16")])
+@pytest.mark.parametrize("T,k,E,h,f,split", [
+    (64, 2, 8, 256, 1024, {"bf16": True, "f32": True}),     # decode-sized: split second product
+    (64, 2, 8, 256, 512, {"bf16": True, "f32": False}),     # fp32 K too short to split (16 steps)
+    (300, 2, 6, 128, 1024, {"bf16": False, "f32": True}),   # 600 rows: split only in fp32 (<= 1024)
+    (700, 3, 5, 64, 256, {"bf16": False, "f32": False}),    # 2100 rows: never split
+    (1, 4, 9, 64, 1024, {"bf16": True, "f32": True}),       # one token
+])
+def test_gather_combine_matches_two_calls(dtype, out_dtype, T, k, E, h, f, split):
+    """moe_expert_ffn_shard_gather_combine = moe_expert_ffn_shard_gather + moe_combine, bit
+    for bit (one launch for the split sum and the combine when K is split, y_perm then left
+    unwritten), and within tolerance of the oracle; dropped picks are skipped."""
+    rng = np.random.default_rng(T * 10 + k + h)
+    x = rng.standard_normal((T, h)).astype(np.float32)
+    w1 = (rng.standard_normal((E, h, f)) * 0.05).astype(np.float32)
+    w2 = (rng.standard_normal((E, f, h)) * 0.05).astype(np.float32)
+    if dtype == "bf16":
+        x, w1, w2 = synth.round_to_bf16(x), synth.round_to_bf16(w1), synth.round_to_bf16(w2)
+    idx = np.stack([rng.permutation(E + 1)[:k] for _ in range(T)]).astype(np.int32)  # id E: dropped
+    wt = rng.uniform(0.1, 1.0, size=(T, k)).astype(np.float32)
+    dt, odt = tdt(dtype), tdt(out_dtype)
+    xd = to_dev(x, dt)
+    packed = moe.pack_weights(to_dev(w1, dt), to_dev(w2, dt), f=f, act="gelu")
+    d = moe.dispatch(to_dev(idx, torch.int32), xd, E, x_perm=False)
+    wd = to_dev(wt, torch.float32)
+    y_perm = moe.expert_ffn_shard_gather(xd, d.row_src, d.offsets, packed, A_max=T * k)
+    y_two = moe.combine(y_perm, d.pos_of, wd, out_dtype=odt)
+    scratch = torch.full((T * k, h), 5.0, dtype=dt, device="cuda")
+    y_one, written = moe.expert_ffn_shard_gather_combine(xd, d.row_src, d.offsets, d.pos_of, wd, packed,
+                                                         y_perm=scratch, out_dtype=odt)
+    torch.cuda.synchronize()
+    ib = torch.int16 if odt == torch.bfloat16 else torch.int32
+    assert torch.equal(y_one.view(ib), y_two.view(ib))
+    assert (written is None) == split[dtype]
+    if split[dtype]:
+        assert bool((scratch == 5.0).all())
+    offsets = d.offsets.cpu().numpy()
+    row_src = d.row_src.cpu().numpy()[:offsets[-1]]
+    ref_perm = oracle.expert_ffn(x[row_src], offsets, w1, None, w2, "gelu")
+    pos = d.pos_of.cpu().numpy()
+    ref = np.zeros((T, h))
+    for j in range(k):  # dropped picks (pos -1) contribute nothing
+        keep = pos[:, j] >= 0
+        ref[keep] += wt[keep, j:j + 1].astype(np.float64) * ref_perm[pos[keep, j]]
+    assert rowwise(np_of(y_one), ref) <= TOL["bf16" if "bf16" in (dtype, out_dtype) else "f32"]
+
+
 @pytest.mark.parametrize("dtype,out_dtype", [("bf16", "bf16"), ("bf16", "f32"), ("f32", "f32")])
 @pytest.mark.parametrize("act", ["gelu", "swiglu"])
 @pytest.mark.parametrize("T,E,h,f", [(700, 6, 256, 200), (90, 3, 72, 128), (1300, 5, 768, 384),
