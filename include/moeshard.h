@@ -109,6 +109,20 @@ moe_status moe_dispatch(const int32_t *topk_idx, int64_t T, int32_t k, int32_t E
                         int32_t *offsets, int32_t *row_src, int32_t *pos_of, void *x_perm,
                         void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* Steps 1 and 2 in one call: moe_route followed by moe_dispatch without x_perm (the grouped
+ * rows are read through row_src by moe_expert_ffn_shard_gather / _top1 / _gather_combine),
+ * with the same outputs bit for bit.  When one routing workgroup covers the whole batch
+ * (bf16, h % 64 == 0, 32 < E <= 256, 1 <= T <= 64, k <= 8: decode-sized batches) that
+ * workgroup also groups the assignments from its picks, in the same launch; otherwise the
+ * two steps run as the two calls would.
+ *   arguments as moe_route and moe_dispatch (ws: moe_dispatch_workspace_size(T, k, E)
+ *   bytes, 16-byte aligned); every argument of both is checked before any launch. */
+moe_status moe_route_dispatch(const void *x, moe_dtype xdt, int64_t T, int64_t h, const void *w_gate,
+                              int32_t E, int32_t k, const float *sel_bias, int64_t bias_row_stride,
+                              int32_t renorm, int32_t *topk_idx, float *topk_w, int32_t *counts,
+                              int32_t *offsets, int32_t *row_src, int32_t *pos_of, void *ws,
+                              size_t ws_bytes, hipStream_t stream);
+
 /* Inner width after padding to the grouped GEMM's tile multiple (the packed layout). */
 int64_t moe_padded_inner_width(int64_t f);
 

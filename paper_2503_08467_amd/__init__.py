@@ -8,4 +8,4 @@ from .layer import (Dispatch, MoEShardLayer, PackedShard, alloc_dispatch, combin
                     dispatch_workspace_size, expert_ffn_shard, expert_ffn_shard_gather,
                     expert_ffn_shard_gather_combine, expert_ffn_shard_noalloc,
                     expert_ffn_shard_per_expert, expert_ffn_shard_top1, ffn_workspace_size, pack_weights,
-                    padded_inner_width, route)
+                    padded_inner_width, route, route_dispatch)

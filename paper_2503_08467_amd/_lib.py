@@ -26,6 +26,8 @@ SIGNATURES = {
     "moe_status_string": (ctypes.c_char_p, [_ST]),
     "moe_route": (_ST, [_P, _ST, _I64, _I64, _P, _I32, _I32, _P, _I64, _I32, _P, _P, _P]),
     "moe_dispatch_workspace_size": (_SZ, [_I64, _I32, _I32]),
+    "moe_route_dispatch": (_ST, [_P, _ST, _I64, _I64, _P, _I32, _I32, _P, _I64, _I32, _P, _P, _P, _P, _P, _P, _P, _SZ,
+                                 _P]),
     "moe_dispatch": (_ST, [_P, _I64, _I32, _I32, _P, _ST, _I64, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "moe_padded_inner_width": (_I64, [_I64]),
     "moe_packed_weights_size": (_SZ, [_I32, _I64, _I64, _ST, _ST]),

@@ -89,6 +89,37 @@ moe_status moe_dispatch(const int32_t* topk_idx, int64_t T, int32_t k, int32_t E
                                          offsets, row_src, pos_of, x_perm, static_cast<int32_t*>(ws), stream));
 }
 
+moe_status moe_route_dispatch(const void* x, moe_dtype xdt, int64_t T, int64_t h, const void* w_gate, int32_t E,
+                              int32_t k, const float* sel_bias, int64_t bias_row_stride, int32_t renorm,
+                              int32_t* topk_idx, float* topk_w, int32_t* counts, int32_t* offsets,
+                              int32_t* row_src, int32_t* pos_of, void* ws, size_t ws_bytes, hipStream_t stream) {
+    // every check of both calls, before any launch
+    if (!valid_dtype(xdt) || T < 0 || !valid_h(h) || !valid_ek(E, k)) return MOE_ERR_INVALID_ARG;
+    if (E > MOE_MAX_EXPERTS) return MOE_ERR_UNSUPPORTED;
+    if (T * k >= INT32_MAX) return MOE_ERR_INVALID_ARG;
+    if (renorm != 0 && renorm != 1) return MOE_ERR_INVALID_ARG;
+    if (bias_row_stride != 0 && bias_row_stride != E) return MOE_ERR_INVALID_ARG;
+    const bool any = T > 0;
+    if (!ok_ptr(x, any) || !ok_ptr(w_gate, true) || !ok_ptr(topk_idx, any) || !ok_ptr(topk_w, any) ||
+        !ok_ptr(counts, true) || !ok_ptr(offsets, true) || !ok_ptr(row_src, any) || !ok_ptr(pos_of, any) ||
+        !ok_ptr(ws, true))
+        return MOE_ERR_INVALID_ARG;
+    if (sel_bias && (reinterpret_cast<uintptr_t>(sel_bias) & 3u)) return MOE_ERR_INVALID_ARG;
+    if (ws_bytes < moe_dispatch_workspace_size(T, k, E)) return MOE_ERR_WORKSPACE;
+    const bool bf16 = xdt == MOE_BF16;
+    if (moe::route_dispatch_fusable(bf16, T, static_cast<int>(h), E, k))
+        return from_hip(moe::launch_route_dispatch(x, T, static_cast<int>(h), w_gate, E, k, sel_bias, bias_row_stride,
+                                                   renorm, topk_idx, topk_w,
+                                                   moe::RouteDispatchOut{counts, offsets, row_src, pos_of}, stream));
+    if (any) {
+        const hipError_t err = moe::launch_route(x, bf16, T, static_cast<int>(h), w_gate, E, k, sel_bias,
+                                                 bias_row_stride, renorm, topk_idx, topk_w, stream);
+        if (err != hipSuccess) return from_hip(err);
+    }
+    return from_hip(moe::launch_dispatch(topk_idx, T, k, E, x, elem_bytes(xdt), static_cast<int>(h), counts, offsets,
+                                         row_src, pos_of, nullptr, static_cast<int32_t*>(ws), stream));
+}
+
 int64_t moe_padded_inner_width(int64_t f) {
     if (f < 1) return 0;
     return (f + moe::kInnerAlign - 1) / moe::kInnerAlign * moe::kInnerAlign;

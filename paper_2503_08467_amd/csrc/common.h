@@ -40,6 +40,18 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
+// Lanes of this wave whose expert equals this lane's (valid lanes only), from nbits ballots
+// over the id bits (E <= 2^nbits).
+__device__ __forceinline__ uint64_t same_expert_lanes(int e, bool valid, int nbits) {
+    uint64_t peers = __ballot(valid);
+    for (int b = 0; b < nbits; ++b) {
+        const bool bit = valid && ((e >> b) & 1);
+        const uint64_t m = __ballot(bit);
+        peers &= bit ? m : ~m;
+    }
+    return peers;
+}
+
 // Activations of the expert FFN (fp32).
 __device__ __forceinline__ float act_gelu(float u) { return 0.5f * u * (1.0f + erff(u * 0.70710678118654752f)); }
 

@@ -294,17 +294,6 @@ __global__ __launch_bounds__(kDispThreads) void dispatch_rank_scan(const int32_t
 
 constexpr int64_t kFusedMaxA = 16384;
 
-// Lanes of this wave whose expert equals this lane's (valid lanes only), from nbits ballots.
-__device__ __forceinline__ uint64_t same_expert_lanes(int e, bool valid, int nbits) {
-    uint64_t peers = __ballot(valid);
-    for (int b = 0; b < nbits; ++b) {
-        const bool bit = valid && ((e >> b) & 1);
-        const uint64_t m = __ballot(bit);
-        peers &= bit ? m : ~m;
-    }
-    return peers;
-}
-
 // One workgroup of 16 waves per chunk of 1024 assignments (one group of 64 per wave), so
 // that counting every assignment is spread over 1024 threads and the chunk is ranked in a
 // single round.

@@ -45,6 +45,24 @@ hipError_t launch_route(const void* x, bool bf16, int64_t T, int h, const void* 
                         const float* bias, int64_t bias_stride, int renorm, int32_t* idx, float* w,
                         hipStream_t s);
 
+// Step 2's outputs written by the routing launch itself (moe_dispatch's counts, offsets,
+// row_src, pos_of; no x_perm).
+struct RouteDispatchOut {
+    int32_t* counts;
+    int32_t* offsets;
+    int32_t* row_src;
+    int32_t* pos_of;
+};
+
+// Whether one routing workgroup covers the whole batch, so that it can also group the
+// assignments: bf16, h % 64 == 0, 32 < E <= 256, 1 <= T <= 64, k <= 8.
+bool route_dispatch_fusable(bool bf16, int64_t T, int h, int E, int k);
+
+// Steps 1 and 2 in one launch (only when route_dispatch_fusable).
+hipError_t launch_route_dispatch(const void* x, int64_t T, int h, const void* wg, int E, int k, const float* bias,
+                                 int64_t bias_stride, int renorm, int32_t* idx, float* w, RouteDispatchOut out,
+                                 hipStream_t s);
+
 hipError_t launch_dispatch(const int32_t* idx, int64_t T, int k, int E, const void* x, int elem_bytes,
                            int h, int32_t* counts, int32_t* offsets, int32_t* row_src,
                            int32_t* pos_of, void* x_perm, int32_t* ws, hipStream_t s);

@@ -11,6 +11,8 @@
 #include "kernels.h"
 #include "lds_dma.h"
 
+#include "../../include/moeshard.h"
+
 namespace moe {
 namespace {
 
@@ -330,6 +332,9 @@ __global__ __launch_bounds__(kWaves * kWave) void route_kernel(const Tin* __rest
 // clamped to the last valid row; their results are never used.
 
 constexpr int kRTok = 64;      // tokens per workgroup
+
+typedef RouteDispatchOut FusedDispatch;  // counts == nullptr: routing only
+constexpr int kFusedGroups = kRTok * kQuadPicks / 64;  // groups of 64 assignments, at most
 constexpr int kRK = 64;        // K elements per chunk (128-byte rows)
 
 template <int NBW>
@@ -354,7 +359,7 @@ __global__ __launch_bounds__(kWaves * kWave) void route_lds_kernel(const bf16_t*
                                                                    const float* __restrict__ bias,
                                                                    int64_t bias_stride, int renorm,
                                                                    int32_t* __restrict__ idx,
-                                                                   float* __restrict__ w) {
+                                                                   float* __restrict__ w, FusedDispatch fd) {
     typedef RouteLds<NBW> S;
     constexpr int EP = S::EP, LPW = S::kLPW, LDW = S::kLDW, NS = S::kStages;
     constexpr int kXJ = kRTok / 8 / 4;  // loads per wave per chunk that carry token rows
@@ -500,11 +505,87 @@ __global__ __launch_bounds__(kWaves * kWave) void route_lds_kernel(const bf16_t*
             w[t * k + q + 4] = renorm ? r.p1 / r.wsum : r.p1;
         }
     }
+    if (fd.counts == nullptr) return;
+
+    // ---- Step 2 in the same launch (this workgroup routed the whole batch): group the A = T k
+    // assignments per expert, stable in (t, j) order -- the same counts, offsets, row_src and
+    // pos_of as moe_dispatch -- from the picks still in registers.  The LDS of the logit
+    // table is reused once every wave is done with it.
+    __syncthreads();
+    int* const sp = reinterpret_cast<int*>(smem);     // [T k] the picks, assignment a = t k + j
+    int* const hist = sp + kRTok * kQuadPicks;         // [E] assignments per expert
+    int* const off = hist + MOE_MAX_EXPERTS;           // [E + 1] exclusive prefix
+    int* const gcnt = off + MOE_MAX_EXPERTS + 1;       // [group][E] count within each group of 64
+    const int A = static_cast<int>(T) * k;
+    if (t < T) {
+        if (q < k) sp[tt * k + q] = r.e0;
+        if (q + 4 < k) sp[tt * k + q + 4] = r.e1;
+    }
+    for (int e = threadIdx.x; e < MOE_MAX_EXPERTS; e += kWaves * kWave) hist[e] = 0;
+    for (int i = threadIdx.x; i < kFusedGroups * MOE_MAX_EXPERTS; i += kWaves * kWave) gcnt[i] = 0;
+    int nbits = 0;
+    while ((1 << nbits) < E) ++nbits;
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    __syncthreads();
+    const int ngroups = (A + 63) / 64;
+    for (int gi = wave; gi < ngroups; gi += kWaves) {  // wave-uniform
+        const int a = gi * 64 + lane;
+        const int e = a < A ? sp[a] : -1;
+        const bool valid = static_cast<unsigned>(e) < static_cast<unsigned>(E);
+        const uint64_t peers = same_expert_lanes(e, valid, nbits);
+        if (valid && __popcll(peers & lt) == 0) {
+            gcnt[gi * MOE_MAX_EXPERTS + e] = __popcll(peers);
+            atomicAdd(&hist[e], __popcll(peers));
+        }
+    }
+    __syncthreads();
+    static_assert(MOE_MAX_EXPERTS == 4 * kWave, "four experts per lane of one wave");
+    if (wave == 0) {
+        int ex[4], sum = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int e = lane * 4 + i;
+            ex[i] = sum;
+            sum += (e < E) ? hist[e] : 0;
+        }
+        int incl = sum;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const int v = __shfl_up(incl, o, kWave);
+            if (lane >= o) incl += v;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int e = lane * 4 + i;
+            if (e < E) off[e] = incl - sum + ex[i];
+        }
+        if (lane == kWave - 1) off[E] = incl;
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e <= E; e += kWaves * kWave) {
+        fd.offsets[e] = off[e];
+        if (e < E) fd.counts[e] = hist[e];
+    }
+    for (int gi = wave; gi < ngroups; gi += kWaves) {
+        const int a = gi * 64 + lane;
+        const int e = a < A ? sp[a] : -1;
+        const bool valid = static_cast<unsigned>(e) < static_cast<unsigned>(E);
+        const uint64_t peers = same_expert_lanes(e, valid, nbits);
+        if (valid) {
+            int pos = off[e] + __popcll(peers & lt);
+            for (int g2 = 0; g2 < gi; ++g2) pos += gcnt[g2 * MOE_MAX_EXPERTS + e];
+            fd.pos_of[a] = pos;
+            fd.row_src[pos] = a / k;
+        } else if (a < A) {
+            fd.pos_of[a] = -1;
+        }
+    }
 }
 
 template <int NBW, int BIAS>
 hipError_t launch_route_lds_b(const void* x, int64_t T, int h, const void* wg, int E, int k, const float* bias,
-                              int64_t bias_stride, int renorm, int32_t* idx, float* w, hipStream_t s) {
+                              int64_t bias_stride, int renorm, int32_t* idx, float* w, FusedDispatch fd,
+                              hipStream_t s) {
     constexpr size_t lds = RouteLds<NBW>::kBytes;
     static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&route_lds_kernel<NBW, BIAS>),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -513,17 +594,17 @@ hipError_t launch_route_lds_b(const void* x, int64_t T, int h, const void* wg, i
     const dim3 grid(static_cast<unsigned>(ceil_div(T, kRTok)));
     hipLaunchKernelGGL((route_lds_kernel<NBW, BIAS>), grid, dim3(kWaves * kWave), lds, s,
                        static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(wg), T, h, E, k, bias, bias_stride,
-                       renorm, idx, w);
+                       renorm, idx, w, fd);
     return hipGetLastError();
 }
 
 template <int NBW>
 hipError_t launch_route_lds(const void* x, int64_t T, int h, const void* wg, int E, int k, const float* bias,
-                            int64_t bias_stride, int renorm, int32_t* idx, float* w, hipStream_t s) {
-    if (!bias) return launch_route_lds_b<NBW, 0>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, s);
+                            int64_t bias_stride, int renorm, int32_t* idx, float* w, FusedDispatch fd, hipStream_t s) {
+    if (!bias) return launch_route_lds_b<NBW, 0>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, fd, s);
     if ((reinterpret_cast<uintptr_t>(bias) & 15u) == 0 && E % 4 == 0 && bias_stride % 4 == 0)
-        return launch_route_lds_b<NBW, 2>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, s);
-    return launch_route_lds_b<NBW, 1>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, s);
+        return launch_route_lds_b<NBW, 2>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, fd, s);
+    return launch_route_lds_b<NBW, 1>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, fd, s);
 }
 
 template <typename Tin, int NB>
@@ -553,17 +634,33 @@ hipError_t launch_route_t(const void* x, int64_t T, int h, const void* wg, int E
 
 }  // namespace
 
-hipError_t launch_route(const void* x, bool bf16, int64_t T, int h, const void* wg, int E, int k,
-                        const float* bias, int64_t bias_stride, int renorm, int32_t* idx, float* w,
-                        hipStream_t s) {
+static hipError_t route_any(const void* x, bool bf16, int64_t T, int h, const void* wg, int E, int k,
+                            const float* bias, int64_t bias_stride, int renorm, int32_t* idx, float* w,
+                            FusedDispatch fd, hipStream_t s) {
     if (T == 0) return hipSuccess;
     if (bf16 && h % kRK == 0 && E > 32) {
-        if (E <= 64) return launch_route_lds<1>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, s);
-        if (E <= 128) return launch_route_lds<2>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, s);
-        return launch_route_lds<4>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, s);
+        if (E <= 64) return launch_route_lds<1>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, fd, s);
+        if (E <= 128) return launch_route_lds<2>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, fd, s);
+        return launch_route_lds<4>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, fd, s);
     }
     return bf16 ? launch_route_t<bf16_t>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, s)
                 : launch_route_t<float>(x, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, s);
+}
+
+hipError_t launch_route(const void* x, bool bf16, int64_t T, int h, const void* wg, int E, int k,
+                        const float* bias, int64_t bias_stride, int renorm, int32_t* idx, float* w,
+                        hipStream_t s) {
+    return route_any(x, bf16, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, FusedDispatch{}, s);
+}
+
+bool route_dispatch_fusable(bool bf16, int64_t T, int h, int E, int k) {
+    return bf16 && h % kRK == 0 && E > 32 && E <= MOE_MAX_EXPERTS && T >= 1 && T <= kRTok && k <= kQuadPicks;
+}
+
+hipError_t launch_route_dispatch(const void* x, int64_t T, int h, const void* wg, int E, int k, const float* bias,
+                                 int64_t bias_stride, int renorm, int32_t* idx, float* w, RouteDispatchOut out,
+                                 hipStream_t s) {
+    return route_any(x, true, T, h, wg, E, k, bias, bias_stride, renorm, idx, w, out, s);
 }
 
 }  // namespace moe

@@ -112,6 +112,37 @@ def dispatch(topk_idx: torch.Tensor, x: torch.Tensor, E: int, out: Optional[Disp
     return out
 
 
+def route_dispatch(x: torch.Tensor, w_gate: torch.Tensor, k: int, sel_bias: Optional[torch.Tensor] = None,
+                   renorm: bool = False, out=None, disp: Optional[Dispatch] = None, ws: Optional[torch.Tensor] = None,
+                   stream=None):
+    """Steps 1 and 2 in one call (one launch for decode-sized batches); the dispatch writes
+    indices only (no x_perm).  Returns (topk_idx, topk_w, Dispatch)."""
+    _dev(x, "x"), _dev(w_gate, "w_gate")
+    T, h = x.shape
+    E = w_gate.shape[0]
+    if w_gate.shape[1] != h or w_gate.dtype != x.dtype:
+        raise ValueError("w_gate must be [E, h] with the dtype of x")
+    stride = 0
+    if sel_bias is not None:
+        _dev(sel_bias, "sel_bias")
+        if sel_bias.dtype != torch.float32:
+            raise TypeError("sel_bias must be float32")
+        stride = 0 if sel_bias.dim() == 1 else E
+        if sel_bias.numel() != (E if stride == 0 else T * E):
+            raise ValueError("sel_bias must be [E] or [T, E]")
+    if out is None:
+        idx = torch.empty((T, k), dtype=torch.int32, device=x.device)
+        w = torch.empty((T, k), dtype=torch.float32, device=x.device)
+    else:
+        idx, w = out
+    if disp is None or ws is None:
+        disp, ws = alloc_dispatch(T, k, E, h, x.dtype, x.device, x_perm=False)
+    _lib.call("moe_route_dispatch", _ptr(x), _dt(x), T, h, _ptr(w_gate), E, k, _ptr(sel_bias), stride,
+              int(bool(renorm)), _ptr(idx), _ptr(w), _ptr(disp.counts), _ptr(disp.offsets), _ptr(disp.row_src),
+              _ptr(disp.pos_of), _ptr(ws), ws.numel(), _stream(x, stream))
+    return idx, w, disp
+
+
 def padded_inner_width(f: int) -> int:
     return int(_lib.load().moe_padded_inner_width(f))
 
@@ -362,10 +393,14 @@ class MoEShardLayer:
             self._alloc(T)
         k = self.k
         idx, w = self.idx[:T], self.w[:T]
-        route(x, self.w_gate, k, sel_bias, self.renorm, out=(idx, w))
         d = Dispatch(self.disp.counts, self.disp.offsets, self.disp.row_src[:T * k], self.disp.pos_of[:T],
                      None if self.disp.x_perm is None else self.disp.x_perm[:T * k])
-        dispatch(idx, x, self.E, out=d, ws=self.dws)
+        if d.x_perm is None:
+            # Steps 1 and 2 in one call (one launch when a single workgroup routes the batch)
+            route_dispatch(x, self.w_gate, k, sel_bias, self.renorm, out=(idx, w), disp=d, ws=self.dws)
+        else:
+            route(x, self.w_gate, k, sel_bias, self.renorm, out=(idx, w))
+            dispatch(idx, x, self.E, out=d, ws=self.dws)
         if d.x_perm is None and k == 1:
             # top-1: the expert step writes the weighted rows straight into y
             y_perm = None

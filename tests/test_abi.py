@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 15, names
+    assert len(names) == 16, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(_lib.SIGNATURES)
@@ -267,3 +267,20 @@ def test_gather_combine_rejects_bad_arguments(lib):
     # no tokens: nothing to launch, nothing written
     assert call(T=0, pos=None, w=None, y=None) == _lib.MOE_OK
     assert flag.value == 1
+
+
+def test_route_dispatch_checks_both_steps_arguments(lib):
+    """The one-call route and dispatch rejects what either call would, before any launch."""
+    T, h, E, k = 64, 128, 64, 2
+    ws = lib.moe_dispatch_workspace_size(T, k, E)
+
+    def call(k=k, E=E, counts=A16, ws_bytes=ws, renorm=0, stride=0):
+        return lib.moe_route_dispatch(A16, _lib.MOE_BF16, T, h, A16, E, k, None, stride, renorm, A16, A16, counts,
+                                      A16, A16, A16, A16, ws_bytes, None)
+    assert call(k=0) == _lib.MOE_ERR_INVALID_ARG
+    assert call(k=E + 1) == _lib.MOE_ERR_INVALID_ARG
+    assert call(E=300, k=2) == _lib.MOE_ERR_UNSUPPORTED
+    assert call(counts=None) == _lib.MOE_ERR_INVALID_ARG
+    assert call(ws_bytes=ws - 1) == _lib.MOE_ERR_WORKSPACE
+    assert call(renorm=2) == _lib.MOE_ERR_INVALID_ARG
+    assert call(stride=5) == _lib.MOE_ERR_INVALID_ARG

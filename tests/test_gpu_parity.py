@@ -80,6 +80,37 @@ def test_route_shapes_and_bias(dtype, T, h, E, k, bias_kind):
     _check_route(x, wg, bias, k, int(k > 1), dtype, dtype == "bf16")
 
 
+@pytest.mark.parametrize("T,h,E,k", [(1, 128, 40, 1), (17, 256, 64, 2), (64, 1024, 64, 2), (64, 128, 128, 8),
+                                     (33, 64, 256, 5), (50, 192, 100, 3),
+                                     (65, 128, 64, 2), (64, 128, 64, 9), (40, 128, 32, 2)])  # separate launches
+@pytest.mark.parametrize("bias_kind", ["none", "row", "shared"])
+def test_route_dispatch_matches_two_calls(T, h, E, k, bias_kind):
+    """moe_route_dispatch = moe_route + moe_dispatch (indices only), every output bit for bit:
+    one launch when a single workgroup routes the batch (T <= 64, k <= 8, 32 < E), the two
+    launches otherwise."""
+    rng = np.random.default_rng(T * 1000 + E + k)
+    x = synth.round_to_bf16(rng.standard_normal((T, h)).astype(np.float32))
+    wg = synth.round_to_bf16((rng.standard_normal((E, h)) * 0.05).astype(np.float32))
+    bias = {"none": None, "row": rng.standard_normal((T, E)).astype(np.float32),
+            "shared": rng.standard_normal(E).astype(np.float32)}[bias_kind]
+    xd, wgd, bd = to_dev(x, torch.bfloat16), to_dev(wg, torch.bfloat16), to_dev(bias, torch.float32)
+    renorm = k > 1
+    idx1, w1 = moe.route(xd, wgd, k, bd, renorm)
+    d1 = moe.dispatch(idx1, xd, E, x_perm=False)
+    d2, ws = moe.alloc_dispatch(T, k, E, h, torch.bfloat16, xd.device, x_perm=False)
+    for key in ("counts", "offsets", "row_src", "pos_of"):
+        getattr(d2, key).fill_(-7)
+    idx2, w2, d2 = moe.route_dispatch(xd, wgd, k, bd, renorm, disp=d2, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(idx1, idx2)
+    assert torch.equal(w1.view(torch.int32), w2.view(torch.int32))
+    n = int(d1.offsets[-1].item())
+    for key in ("counts", "offsets", "pos_of"):
+        assert torch.equal(getattr(d1, key), getattr(d2, key)), key
+    assert torch.equal(d1.row_src[:n], d2.row_src[:n])
+    assert np.array_equal(d2.counts.cpu().numpy(), np.bincount(idx2.cpu().numpy().ravel(), minlength=E))
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_route_exact_ties_go_to_lower_expert(dtype):
     rng = np.random.default_rng(5)
