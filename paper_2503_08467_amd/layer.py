@@ -1,4 +1,4 @@
-"""Python face of the C ABI: the four calls of the layer plus the one-time shard packing.
+"""Python face of the C ABI: the calls of the layer plus the one-time shard packing.
 
 Argument marshalling only -- every step of the layer runs in the HIP kernels of
 libmoeshard.so.  Tensors must be contiguous CUDA (HIP) tensors; torch provides the device
@@ -356,8 +356,10 @@ def combine(y_perm: torch.Tensor, pos_of: torch.Tensor, topk_w: torch.Tensor,
 class MoEShardLayer:
     """One device's MoE layer: replicated gate + this device's shard of every expert.
 
-    forward() issues the four library calls on the current stream into buffers that are
-    allocated once for a maximum token count.
+    forward() issues the library calls on the current stream into buffers that are
+    allocated once for a maximum token count: with fused_gather (the default) routing and
+    grouping in one call, then the expert step with the combine in one call (top-1: the
+    expert step writing y); without it route, dispatch with x_perm, expert step, combine.
     """
 
     def __init__(self, w_gate: torch.Tensor, packed: PackedShard, k: int, renorm: bool = False,
