@@ -349,11 +349,11 @@ def main():
 
     top1_fused = cfg.k == 1 and not args.unfused_gather
 
-    def step(ev=None, ffn_ev=None):
-        """One layer forward.  ev: 5 events around the four calls (stage breakdown: routing
-        and grouping as separate calls); ffn_ev: 2 events around the expert-FFN call only.
-        Without ev, routing and grouping run as the one call the layer uses (moe_route_dispatch,
-        one launch for decode-sized batches) whenever no x_perm is written."""
+    def step_parts(ev=None, ffn_ev=None):
+        """One layer forward as separate calls, for the measurements that need events between
+        them.  ev: 5 events around route, dispatch, expert step and combine (stage breakdown);
+        ffn_ev: 2 events around the expert-step call only (the expert step alone: the combine
+        stays a call of its own)."""
         T, k = cfg.T, cfg.k
         if ev is None and layer.disp.x_perm is None:
             moe.route_dispatch(x, wg, k, bias, bool(cfg.renorm), out=(layer.idx, layer.w), disp=layer.disp,
@@ -380,6 +380,10 @@ def main():
             moe.combine(layer.y_perm, layer.disp.pos_of, layer.w, out=layer.y)
         if ev: ev[4].record(stream)
 
+    def step():
+        """One layer forward exactly as MoEShardLayer runs it (its calls, its buffers)."""
+        layer(x, bias)
+
     def new_events(n, m):
         return [[torch.cuda.Event(enable_timing=True) for _ in range(m)] for _ in range(n)]
 
@@ -390,58 +394,86 @@ def main():
         return {"median": round(float(np.median(v)), 2), "p10": round(float(np.percentile(v, 10)), 2),
                 "p90": round(float(np.percentile(v, 90)), 2)}
 
-    # cache flush: 512 MiB written (more than L2 and MALL together), outside the step's events
-    scratch = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device=dev)
+    # Cache flush, outside the step's events: 512 MiB (more than L2 and MALL together) written,
+    # then read back.  The read pass leaves the caches holding clean lines of the scratch
+    # buffer only; after the write alone they would hold dirty lines whose write-back to HBM
+    # then runs inside the next step (a cost of the flush, not of the layer; the step time
+    # after a write-only flush is reported separately).
+    scratch = torch.empty(128 * 1024 * 1024, dtype=torch.float32, device=dev)
+    flush_sum = torch.empty((), dtype=torch.float32, device=dev)
+
+    def flush(i, read_back=True):
+        scratch.fill_(float(i & 0xff))
+        if read_back:
+            torch.sum(scratch, dim=0, out=flush_sum)
 
     # untimed warm-up steps, each after a flush like the timed ones; their step times are kept
     # (events around the step only) to show how the step time settles
     wev = new_events(args.warmup, 2)
     for i in range(args.warmup):
-        scratch.fill_(i & 0xff)
+        flush(i)
         wev[i][0].record(stream)
         step()
         wev[i][1].record(stream)
+    step_parts(ffn_ev=new_events(1, 2)[0])  # first use of the separate calls (host-side setup)
     torch.cuda.synchronize()
     warm_curve = us(wev) if args.warmup else np.zeros(0)
 
     # the timed steps: every step starts with cold caches (a flush before it, outside its
-    # events); value = tokens over the summed step times
-    sev, fev = new_events(args.steps, 2), new_events(args.steps, 2)
+    # events); value = tokens over the summed step times.  No event inside a step: each event
+    # record leaves the GPU idle for a few microseconds.
+    sev = new_events(args.steps, 2)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        scratch.fill_((i + 1) & 0xff)
+        flush(i + 1)
         sev[i][0].record(stream)
-        step(ffn_ev=fev[i])
+        step()
         sev[i][1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    step_each, ffn_each = us(sev), us(fev)
-    del scratch
+    step_each = us(sev)
+
+    # the same steps after a write-only flush (dirty lines left in L2 and MALL)
+    dev_ = new_events(args.steps, 2)
+    for i in range(args.steps):
+        flush(i + 1, read_back=False)
+        dev_[i][0].record(stream)
+        step()
+        dev_[i][1].record(stream)
+    torch.cuda.synchronize()
+    dirty_each = us(dev_)
+
+    # the expert step's own time: as many cold-cache steps again, made of the separate calls
+    # with events around the expert-step call (the roofline's kernel time)
+    fev = new_events(args.steps, 2)
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        flush(i + 1)
+        step_parts(ffn_ev=fev[i])
+    torch.cuda.synchronize()
+    ffn_each = us(fev)
 
     # warm caches: back-to-back steps, wall clock (an extra figure, not the headline)
     warm = None
     if args.warm_steps:
-        wfe = new_events(args.warm_steps, 2)
         torch.cuda.synchronize()
         tw = time.perf_counter()
         for i in range(args.warm_steps):
-            step(ffn_ev=wfe[i])
+            step()
         torch.cuda.synchronize()
         wall_w = time.perf_counter() - tw
         warm = {"steps": args.warm_steps, "tokens_per_s": round(cfg.T * args.warm_steps / wall_w, 1),
                 "ms_per_step": round(wall_w / args.warm_steps * 1e3, 4),
-                "expert_ffn_us": spread(us(wfe)),
                 "note": "back-to-back steps without a flush, wall clock; inputs and weights partly in L2/MALL"}
 
     # stage breakdown from a separate, untimed pass (its events add gaps between calls)
     nbrk = min(args.steps, 10)
     events = new_events(nbrk + 1, 5)
-    scratch = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device=dev)
-    step(ev=events.pop())  # the separate route and dispatch calls' first use (host-side setup), not counted
+    step_parts(ev=events.pop())  # the separate route and dispatch calls' first use (host-side setup)
     for i in range(nbrk):
-        scratch.fill_(i & 0xff)
-        step(ev=events[i])
+        flush(i)
+        step_parts(ev=events[i])
     torch.cuda.synchronize()
     del scratch
     stage = np.zeros(4)
@@ -474,8 +506,9 @@ def main():
     roof["traffic"] = measured_traffic(args.config)
     roof["kernel"] = ("moe_expert_ffn_shard" + ("_top1" if top1_fused else "" if args.unfused_gather else "_gather") +
                       " (grouped GEMM1+act and GEMM2, one launch each; calls of at most 512 bf16 rows"
-                      " add one launch that sums the K parts of GEMM2); HIP events around the call in every "
-                      "timed (cold-cache) step")
+                      " add one launch that sums the K parts of GEMM2); HIP events around the call in a "
+                      "second pass of as many cold-cache steps as the timed ones, made of the layer's calls "
+                      "one by one (the timed steps carry no event inside them)")
     roof["algorithmic"] = {"bytes": ffn_bytes, "flops": ffn_flops, "touched_experts": touched,
                            "mfma_util": round(achieved_tflops / peak_tf, 4),
                            "hbm_frac": round(achieved_gbs / PEAK_HBM_GBS, 4)}
@@ -507,9 +540,13 @@ def main():
                                f"({cfg.act}), routing {cfg.routing[0]}",
                    "tokens": cfg.T, "hidden": h, "experts": cfg.E, "top_k": cfg.k, "shard_inner_width": f,
                    "parallelism": "single device"},
-        "timing": ("cold caches: 512 MiB written before every timed step, outside HIP events that bracket the "
-                   "step; value = tokens / mean step time; wall clock of the timed loop (flushes included) "
-                   f"{wall * 1e3:.2f} ms"),
+        "timing": ("cold caches: 512 MiB written and read back before every timed step, outside HIP events that "
+                   "bracket the step (MoEShardLayer.forward, no event inside it); value = tokens / mean step "
+                   f"time; wall clock of the timed loop (flushes included) {wall * 1e3:.2f} ms"),
+        "after_write_only_flush": {"step_us": spread(dirty_each),
+                                   "tokens_per_s": round(cfg.T / (float(np.mean(dirty_each)) * 1e-6), 1),
+                                   "note": "the same steps after a flush that writes 512 MiB without reading it "
+                                           "back: the write-back of its dirty lines runs inside the step"},
         "stages_us": {"route": round(stage_us[0], 2), "dispatch": round(stage_us[1], 2),
                       "expert_ffn": round(stage_us[2], 2), "combine": round(stage_us[3], 2),
                       "note": "separate untimed pass with events between calls" +
