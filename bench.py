@@ -297,7 +297,7 @@ def main():
     ap.add_argument("--config", default="c5")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--warm-steps", type=int, default=20,
+    ap.add_argument("--warm-steps", type=int, default=50,
                     help="after the timed (cold-cache) steps, this many back-to-back steps with warm caches")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run an untimed plain copy of this size first (counter calibration)")
@@ -457,6 +457,8 @@ def main():
     # warm caches: back-to-back steps, wall clock (an extra figure, not the headline)
     warm = None
     if args.warm_steps:
+        for _ in range(5):  # untimed: the clock and the caches settle after the host's pause
+            step()
         torch.cuda.synchronize()
         tw = time.perf_counter()
         for i in range(args.warm_steps):
