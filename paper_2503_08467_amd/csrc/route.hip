@@ -256,8 +256,13 @@ struct StridedExperts {
 template <int NB>
 constexpr int route_ldw() { return NB * 32 + 8; }  // padded row: 8 token rows hit 8 bank groups
 
+// Waves of route_kernel: 8 (each a K eighth) when its partial logits fit LDS comfortably,
+// else 4.  The first four waves run the epilogue.
+template <int NB>
+constexpr int route_waves() { return NB <= 2 ? 8 : kWaves; }
+
 template <typename Tin, int NB>
-__global__ __launch_bounds__(kWaves * kWave) void route_kernel(const Tin* __restrict__ x,
+__global__ __launch_bounds__(route_waves<NB>() * kWave) void route_kernel(const Tin* __restrict__ x,
                                                                const Tin* __restrict__ wg, int64_t T, int h,
                                                                int E, int k, const float* __restrict__ bias,
                                                                int64_t bias_stride, int renorm,
@@ -266,24 +271,40 @@ __global__ __launch_bounds__(kWaves * kWave) void route_kernel(const Tin* __rest
     constexpr int LDW = route_ldw<NB>();
     constexpr int U = (NB == 1) ? 8 : (NB == 2) ? 4 : 2;  // K chunks in flight per wave
     constexpr int NV = EP / 8;                             // experts per lane in the epilogue
-    extern __shared__ float part[];                        // [kWaves][kTok][LDW] partial logits
+    constexpr int RW = route_waves<NB>();
+    extern __shared__ float part[];                        // [RW][kTok][LDW] partial logits
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const int64_t tok0 = static_cast<int64_t>(blockIdx.x) * kTok;
     const int r = lane & 31, g = lane >> 5;
 
     typedef GateFrag<Tin> F;
+    // The epilogue's token and experts of this lane (waves 0..3): token tt, experts q, q + 8,
+    // ...  Their selection bias is loaded now, from clamped addresses (entries past T or E
+    // are loaded but never used), so that its latency hides behind the K loop instead of
+    // costing a round trip per expert at the end.
+    const int tt = wave * 8 + (lane >> 3), q = lane & 7;
+    const int64_t t = tok0 + tt;
+    float bv[NV];
+#pragma unroll
+    for (int j = 0; j < NV; ++j) bv[j] = 0.f;
+    if (bias && wave < kTok / 8) {
+        const float* bp = bias + (t < T ? t : T - 1) * bias_stride;
+#pragma unroll
+        for (int j = 0; j < NV; ++j) bv[j] = bp[min(q + 8 * j, E - 1)];
+    }
+
     f32x16_t acc[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[nb][i] = 0.f;
 
-    for (int k0 = wave * F::kStep; k0 < h; k0 += kWaves * U * F::kStep) {
+    for (int k0 = wave * F::kStep; k0 < h; k0 += RW * U * F::kStep) {
         typename F::frag_t a[U], b[U][NB];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int kk = F::lane_k(k0 + u * kWaves * F::kStep, g);
+            const int kk = F::lane_k(k0 + u * RW * F::kStep, g);
             a[u] = F::load(x, tok0 + r, T, h, kk);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) b[u][nb] = F::load(wg, nb * 32 + r, E, h, kk);
@@ -303,18 +324,19 @@ __global__ __launch_bounds__(kWaves * kWave) void route_kernel(const Tin* __rest
         for (int i = 0; i < 16; ++i) mine[(8 * (i >> 2) + 4 * g + (i & 3)) * LDW + nb * 32 + r] = acc[nb][i];
     __syncthreads();
 
+    if (wave >= kTok / 8) return;
     // eight lanes per token: lane q = lane & 7 holds experts q, q + 8, q + 16, ...
-    const int tt = wave * 8 + (lane >> 3), q = lane & 7;
-    const int64_t t = tok0 + tt;
     float lv[NV], sv[NV];
 #pragma unroll
     for (int j = 0; j < NV; ++j) {
         const int e = q + 8 * j;
         const int o = tt * LDW + e;
-        const float v = ((part[o] + part[kTok * LDW + o]) + part[2 * kTok * LDW + o]) + part[3 * kTok * LDW + o];
+        float v = part[o];  // the waves' partial sums in wave order
+#pragma unroll
+        for (int p = 1; p < RW; ++p) v += part[p * kTok * LDW + o];
         const bool ok = e < E;
         lv[j] = ok ? v : -INFINITY;
-        sv[j] = ok ? ((bias && t < T) ? v + bias[t * bias_stride + e] : v) : -INFINITY;
+        sv[j] = ok ? v + bv[j] : -INFINITY;  // bv = 0 without a bias
     }
     const Picks pk = select_token<NV, StridedExperts<NV>>(lv, sv, q, E, k, renorm, t < T, t, idx, w);
     store_pick(pk, q, k, renorm, t < T, t, idx, w);
@@ -611,14 +633,14 @@ template <typename Tin, int NB>
 hipError_t launch_route_nb(const void* x, int64_t T, int h, const void* wg, int E, int k, const float* bias,
                            int64_t bias_stride, int renorm, int32_t* idx, float* w, hipStream_t s) {
     const dim3 grid(static_cast<unsigned>(ceil_div(T, kTok)));
-    const size_t lds = sizeof(float) * kWaves * kTok * route_ldw<NB>();
+    const size_t lds = sizeof(float) * route_waves<NB>() * kTok * route_ldw<NB>();
     if (lds > 64 * 1024) {
         static hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&route_kernel<Tin, NB>),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize,
                                                      static_cast<int>(lds));
         if (attr != hipSuccess) return attr;
     }
-    hipLaunchKernelGGL((route_kernel<Tin, NB>), grid, dim3(kWaves * kWave), lds, s, static_cast<const Tin*>(x),
+    hipLaunchKernelGGL((route_kernel<Tin, NB>), grid, dim3(route_waves<NB>() * kWave), lds, s, static_cast<const Tin*>(x),
                        static_cast<const Tin*>(wg), T, h, E, k, bias, bias_stride, renorm, idx, w);
     return hipGetLastError();
 }
