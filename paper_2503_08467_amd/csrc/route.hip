@@ -1,12 +1,13 @@
 // Step 1 of the layer: gate logits, top-k selection and softmax weights.
 //
-// A workgroup of four waves routes 32 tokens.  The gate product
-// logits[t, e] = x[t] . w_gate[e] runs on MFMA 32x32 blocks with fp32 accumulation; the
-// K dimension is split across the four waves (wave w takes K chunks w, w + 4, ...), each
-// wave keeping its 32 x E_pad partial block in accumulators with several chunks' loads in
-// flight.  The partials meet in LDS and are summed in a fixed order.  Each token is then
-// reduced by eight lanes: max and sum of exponentials for the softmax, then k rounds of
-// arg-max over logit + bias in which the lower expert id wins ties.
+// route_kernel: a workgroup of RW waves (8 for at most 64 experts, else 4) routes 32
+// tokens.  The gate product logits[t, e] = x[t] . w_gate[e] runs on MFMA 32x32 blocks with
+// fp32 accumulation; the K dimension is split across the waves (wave w takes K chunks w,
+// w + RW, ...), each wave keeping its 32 x E_pad partial block in accumulators with several
+// chunks' loads in flight.  The partials meet in LDS and are summed in wave order.  Each
+// token is then reduced by eight lanes of the first four waves: max and sum of exponentials
+// for the softmax, then k rounds of arg-max over logit + bias in which the lower expert id
+// wins ties.  route_lds_kernel (bf16, h % 64 == 0, more than 32 experts) is described below.
 #include "common.h"
 #include "kernels.h"
 #include "lds_dma.h"
