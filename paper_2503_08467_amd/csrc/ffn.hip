@@ -7,20 +7,20 @@
 //
 // Each workgroup first turns offsets[] into a per-expert prefix of row tiles, then maps
 // linear tile ids to (expert, row tile, column tile).  The grid is persistent (sized from
-// the host-known bound A_max, at most two workgroups per CU, a multiple of the 8 XCDs), so
-// the counts are never read back to the host.
+// the host-known bound A_max, at most as many workgroups per CU as LDS allows, a multiple
+// of the 8 XCDs), so the counts are never read back to the host.
 //
 // bf16 path (gemm_bf16_lds, gemm_up_pairs): 128-row tiles, 256 (or 384 / 128) weight rows
 // per tile, v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  Weights and H are stored
 // K-blocked (blocks of 32 K values, all rows side by side), so every stage of 32 K values
 // of a run of rows is one contiguous stretch that 1 KiB direct-to-LDS loads fetch; three
 // LDS stages, two in flight across K steps and tiles.  The epilogue applies the activation
-// in fp32, rounds once, and stores 8-byte vectors straight from the accumulators (into
+// in fp32, rounds once, and stores 16-byte runs straight from the accumulators (into
 // K-blocked H for GEMM1).  Calls of at most 512 rows split GEMM2's K into parts summed by
-// split_reduce in a fixed order.
+// split_reduce (or, with the combine folded in, split_combine) in a fixed order.
 // fp32 path (gemm_f32_lds): 32 x 128 tiles on v_mfma_f32_32x32x2_f32, row-major operands in
-// 128-byte row pieces through three direct-to-LDS stages; gemm_f32 (register-staged 64 x 64
-// tiles) only for an up-projection whose h is not a multiple of 32.
+// 128-byte row pieces through two direct-to-LDS stages, three workgroups per CU; gemm_f32
+// (register-staged 64 x 64 tiles) only for an up-projection whose h is not a multiple of 32.
 #include "common.h"
 #include "kernels.h"
 #include "lds_dma.h"
