@@ -48,10 +48,15 @@ FFN_SOURCES = ["paper_2503_08467_amd/csrc/ffn.hip", "paper_2503_08467_amd/csrc/c
 
 
 def ffn_source_hash() -> str:
+    """Hash of the expert-step sources as the compiler sees them: line comments and blank
+    lines left out, so that a comment edit does not orphan the committed counter figures."""
     h = hashlib.sha256()
     for p in FFN_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, p), encoding="utf-8") as fh:
+            for line in fh:
+                code = line.split("//", 1)[0].rstrip()
+                if code:
+                    h.update(code.encode() + b"\n")
     return h.hexdigest()[:16]
 
 
