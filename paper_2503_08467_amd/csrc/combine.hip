@@ -45,6 +45,8 @@ struct Row8<false> {
     }
 };
 
+constexpr int kCombineUnroll = 4;  // picks whose rows are loaded together
+
 template <bool YB, bool OB>
 __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ y_perm,
                                                       const int32_t* __restrict__ pos_of,
@@ -56,14 +58,42 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ y
     const int64_t t = i / nv;
     const int c = static_cast<int>(i - t * nv) * 8;
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int j = 0; j < k; ++j) {
-        const int32_t p = pos_of[t * k + j];
-        if (p < 0 || p >= T * k) continue;
-        const float wt = w[t * k + j];
-        float v[8];
-        Row8<YB>::load(y_perm, static_cast<int64_t>(p) * h + c, v);
+    if (k <= kCombineUnroll) {
+        // every position and weight first, then every row from a clamped position (a load
+        // behind a per-lane condition would wait for each row in turn); rows of positions out
+        // of range are loaded but not added
+        int32_t pos[kCombineUnroll];
+        float wt[kCombineUnroll];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) acc[q] += wt * v[q];
+        for (int j = 0; j < kCombineUnroll; ++j)
+            if (j < k) {
+                pos[j] = pos_of[t * k + j];
+                wt[j] = w[t * k + j];
+            }
+        float v[kCombineUnroll][8];
+#pragma unroll
+        for (int j = 0; j < kCombineUnroll; ++j)
+            if (j < k) {
+                const bool ok = pos[j] >= 0 && pos[j] < T * k;
+                Row8<YB>::load(y_perm, static_cast<int64_t>(ok ? pos[j] : 0) * h + c, v[j]);
+            }
+#pragma unroll
+        for (int j = 0; j < kCombineUnroll; ++j)
+            if (j < k) {
+                const bool ok = pos[j] >= 0 && pos[j] < T * k;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) acc[q] = ok ? acc[q] + wt[j] * v[j][q] : acc[q];
+            }
+    } else {
+        for (int j = 0; j < k; ++j) {
+            const int32_t p = pos_of[t * k + j];
+            if (p < 0 || p >= T * k) continue;
+            const float wt = w[t * k + j];
+            float v[8];
+            Row8<YB>::load(y_perm, static_cast<int64_t>(p) * h + c, v);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) acc[q] += wt * v[q];
+        }
     }
     Row8<OB>::store(y, t * h + c, acc);
 }
