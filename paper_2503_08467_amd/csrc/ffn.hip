@@ -78,11 +78,15 @@ __device__ __forceinline__ int tile_prefix(const int32_t* __restrict__ offsets, 
     static_assert(MOE_MAX_EXPERTS == 4 * 64, "four experts per lane of one wave");
     if (threadIdx.x < 64) {
         const int lane = threadIdx.x;
+        // offsets of the lane's four experts and the next, all loaded before any is used
+        // (from clamped indices: a load behind a per-lane condition waits for itself)
+        int o[5];
+#pragma unroll
+        for (int i = 0; i < 5; ++i) o[i] = offsets[min(lane * 4 + i, E)];
         int ex[4], run = 0;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int e = lane * 4 + i;
-            const int cnt = (e < E) ? offsets[e + 1] - offsets[e] : 0;
+            const int cnt = (lane * 4 + i < E) ? o[i + 1] - o[i] : 0;
             ex[i] = run;
             run += cnt > 0 ? (cnt + BM - 1) / BM : 0;
         }
@@ -423,11 +427,13 @@ struct RegTiles {
         static_assert(MOE_MAX_EXPERTS == 4 * 64, "four experts per lane of one wave");
         E = num_experts;
         const int lane = threadIdx.x & 63;
+        int o[5];  // loaded together from clamped indices, as in tile_prefix
+#pragma unroll
+        for (int i = 0; i < 5; ++i) o[i] = offsets[min(lane * 4 + i, num_experts)];
         int run = 0;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int e = lane * 4 + i;
-            const int cnt = (e < E) ? offsets[e + 1] - offsets[e] : 0;
+            const int cnt = (lane * 4 + i < E) ? o[i + 1] - o[i] : 0;
             ex[i] = run;
             run += cnt > 0 ? (cnt + BM - 1) / BM : 0;
         }
