@@ -513,6 +513,17 @@ __device__ __forceinline__ TileGeom tile_geom(const GroupedGemm& g, const Tiles&
     return t;
 }
 
+// Last activation row of a tile worth loading: rows past the tile's valid ones then load that
+// row again (their results are never stored), so that a mostly empty tile's loads touch one
+// line each.  A tile shifted back at the end of the buffer keeps the buffer's limit.
+template <int BM>
+__device__ __forceinline__ int tile_row_limit(const GroupedGemm& g, const TileGeom& t) {
+    const int lim = static_cast<int>(g.rows_max < BM ? g.rows_max : BM) - 1;
+    if (t.row_base != t.row0) return lim;
+    const int64_t valid = t.row_end - t.row0;
+    return valid >= 1 && valid - 1 < lim ? static_cast<int>(valid - 1) : lim;
+}
+
 // Persistent grouped GEMM.  The grid is a fixed number of workgroups (one or two per CU);
 // the tiles are dealt to the 8 XCDs in contiguous runs (the hardware deals workgroups
 // round-robin, so workgroup b sits on XCD b % 8) and, inside a run, round-robin to that
@@ -593,7 +604,7 @@ void gemm_bf16_lds(GroupedGemm g) {
             // this lane's activation rows come from the gathered source rows (the index
             // load makes the compiler wait for the loads in flight: once per tile)
             const int r_lane = lane / CPR, c_lane = lane % CPR;
-            const int a_lim = static_cast<int>(g.rows_max < BM ? g.rows_max : BM) - 1;
+            const int a_lim = tile_row_limit<BM>(g, t);
 #pragma unroll
             for (int j = 0; j < kAJ; ++j) {
                 const int R = (j * NW + wave) * RPI + r_lane;
@@ -603,6 +614,14 @@ void gemm_bf16_lds(GroupedGemm g) {
             }
             src_a = uniform_ptr(g.a);
         } else {
+            const int r_lane = lane / CPR, c_lane = lane % CPR;
+            const int a_lim = tile_row_limit<BM>(g, t);
+#pragma unroll
+            for (int j = 0; j < kAJ; ++j) {
+                const int R = (j * NW + wave) * RPI + r_lane;
+                const int kc = c_lane ^ ((R >> SH) & (CPR - 1));
+                voff[j] = static_cast<uint32_t>(min(R, a_lim)) * static_cast<uint32_t>(rb) + static_cast<uint32_t>(kc * 16);
+            }
             src_a = uniform_ptr(static_cast<const unsigned char*>(g.a) + t.row_base * rb +
                                 (kUp ? 0 : k0 * g.rows_max * 64));
         }
@@ -897,7 +916,8 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_up_pairs(GroupedGemm g) {
             const int c = (lane & 7) ^ (R & 7);
             // gathered: absolute source row (T h s < 4 GiB is checked by the host); else the
             // tile's base carries the row offset
-            const int64_t r = g.gather ? source_row(g, t.row_base + min(R, a_lim)) : min(R, a_lim);
+            const int a_lim_t = tile_row_limit<BM>(g, t);
+            const int64_t r = g.gather ? source_row(g, t.row_base + min(R, a_lim_t)) : min(R, a_lim_t);
             voffA[j] = static_cast<uint32_t>(r) * static_cast<uint32_t>(2 * g.K) + static_cast<uint32_t>(c * 16);
         }
         src_a = uniform_ptr(static_cast<const unsigned char*>(g.a) + (g.gather ? 0 : t.row_base * 2 * g.K));
