@@ -1,7 +1,8 @@
 """Benchmark of the sharded expert-FFN MoE layer on one MI355X.
 
-One step = one full layer forward (route -> dispatch -> expert FFN shard -> combine) over
-one batch of synthetic tokens already resident in HBM.  Prints one JSON line.
+One step = one full layer forward (route -> dispatch -> expert FFN shard -> combine, as
+MoEShardLayer.forward issues it) over one batch of synthetic tokens already resident in
+HBM, every timed step after a 512 MiB write + read-back cache flush.  Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--config c5] [--no-cpu-baseline] [--warm-steps N]
   python bench.py --ablation        # grouped vs per-expert launches, E = 8 .. 256
